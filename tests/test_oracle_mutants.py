@@ -1,0 +1,115 @@
+"""The oracle's pins catch plausible mistakes (CPU only).
+
+Each case plants one mistake in a copy of the oracle's C source, compiles it
+and runs a reduced set of the pins on it; every mutant must fail at least one.
+The unmodified source must pass the same set, so the check itself is sound.
+"""
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import bruteforce as bf
+import oracle as orc
+from oracle import build as obuild
+from test_oracle_conv import ref_conv
+
+SRC = open(obuild.SRC).read()
+
+MUTANTS = {
+    "ties_away": ("int round_up = half_bit && (below_half || (sig & 1));", "int round_up = half_bit;"),
+    "truncate": ("int round_up = half_bit && (below_half || (sig & 1));", "int round_up = 0;"),
+    "sticky_dropped": ("int below_half = big_any_below(M, k - 1);", "int below_half = 0;"),
+    "no_renormalise": ("sig >>= 1;\n      u += 1;", "sig >>= 1;"),
+    "bias_off_by_one": ("return ((int64_t)1 << (f.wE - 1)) - 1;", "return ((int64_t)1 << (f.wE - 1));"),
+    "E0_reserved": ("if (Eb < 0) return make_zero(s, f);", "if (Eb < 1) return make_zero(s, f);"),
+    "Emax_reserved": ("if (Eb > (((int64_t)1 << f.wE) - 1)) return make_inf(s, f);",
+                      "if (Eb >= (((int64_t)1 << f.wE) - 1)) return make_inf(s, f);"),
+    "cancel_sign": ("if (c == 0) return make_zero(0, f);", "if (c == 0) return make_zero(A.s, f);"),
+    "zero_zero_sign": ("make_zero(A.s & B.s, f)", "make_zero(A.s | B.s, f)"),
+    "zero_times_inf": ("if ((A.exn == EXN_INF && B.exn == EXN_ZERO) || (A.exn == EXN_ZERO && B.exn == EXN_INF))",
+                       "if (0)"),
+    "inf_minus_inf": ("return A.s == B.s ? make_inf(A.s, f) : make_nan(f);", "return make_inf(A.s, f);"),
+    "sub_sign": ("      s = B.s;", "      s = A.s;"),
+    "product_exponent": ("exp2_of(A, fi) + exp2_of(B, fi));", "exp2_of(A, fi) + exp2_of(B, fi) + 1);"),
+    "align_wrong_operand": ("big_set_shl(&Y, sig_of(B, f), (int)(eb - emin));",
+                            "big_set_shl(&Y, sig_of(B, f), (int)(ea - emin));"),
+    "relu_keeps_neg_zero": ("if (A.s) return make_zero(0, f);",
+                            "if (A.s && A.exn != EXN_ZERO) return make_zero(0, f);"),
+    "nan_sign": ("static uint64_t make_nan(fmt_t f) { return encode(EXN_NAN, 0, 0, 0, f); }",
+                 "static uint64_t make_nan(fmt_t f) { return encode(EXN_NAN, 1, 0, 0, f); }"),
+    "subnormal_scale": ("int64_t e = ef ? (int64_t)ef - 150 : -149;", "int64_t e = ef ? (int64_t)ef - 150 : -150;"),
+    "channel_order": ("for (int c = 0; c < d->C; c++) {", "for (int c = d->C - 1; c >= 0; c--) {"),
+    "padding_index": ("int ix = ox * d->stride + kx - d->pad;", "int ix = ox * d->stride + kx;"),
+    "relu_after_convert": ("  if (d->act == 1) acc = hfo_relu(acc, d->wE, d->wF_acc);\n  return hfo_convert(acc, d->wE, d->wF_acc, d->wF_out);",
+                           "  return hfo_convert(acc, d->wE, d->wF_acc, d->wF_out);"),
+}
+
+
+def compile_variant(tmp_path, name, src):
+    c = tmp_path / f"{name}.c"
+    c.write_text(src)
+    so = tmp_path / f"{name}.so"
+    subprocess.run(["gcc", "-std=c11", "-O1", "-fPIC", "-shared", "-pthread", "-I",
+                    os.path.dirname(obuild.SRC), "-o", str(so), str(c), "-lm"], check=True)
+    return orc.load(str(so))
+
+
+@pytest.fixture(scope="module")
+def refs():
+    r = {}
+    n = 1 << 11
+    a = np.repeat(np.arange(n, dtype=np.uint64), n)
+    b = np.tile(np.arange(n, dtype=np.uint64), n)
+    r["mul"] = (a, b, bf.mul(a, b, 5, 3, 4))
+    n = 1 << 10
+    a2 = np.repeat(np.arange(n, dtype=np.uint64), n)
+    b2 = np.tile(np.arange(n, dtype=np.uint64), n)
+    r["add"] = (a2, b2, bf.add(a2, b2, 4, 3))
+    cv = np.arange(1 << 12, dtype=np.uint64)
+    r["relu"] = (cv, bf.relu(cv, 5, 4))
+    g = np.random.default_rng(3)
+    x = np.concatenate([g.integers(0, 1 << 32, 1 << 16, dtype=np.uint64).astype(np.uint32).view(np.float32),
+                        np.array([1e-40, 3e-39, -2e-39], np.float32)])
+    r["q"] = (x, bf.quantize(x, 5, 3), bf.quantize(x, 8, 7))
+    ifm = bf.quantize(g.uniform(-2, 2, (1, 5, 6, 4)).astype(np.float32), 5, 3)
+    w = bf.quantize(g.uniform(-1, 1, (3, 3, 4, 3)).astype(np.float32), 5, 3)
+    r["conv"] = (ifm, w, ref_conv(ifm, w, 1, 1, 5, 3, 4, 4), ref_conv(ifm, w, 1, 1, 5, 3, 4, 4, act=1))
+    return r
+
+
+def failures(L, r):
+    """Names of the reduced pins that library L fails."""
+    bad = []
+    a, b, want = r["mul"]
+    if not np.array_equal(orc.mul(a, b, 5, 3, 4, L=L), want):
+        bad.append("mul")
+    a, b, want = r["add"]
+    if not np.array_equal(orc.add(a, b, 4, 3, L=L), want):
+        bad.append("add")
+    cv, want = r["relu"]
+    if not np.array_equal(orc.relu(cv, 5, 4, L=L), want):
+        bad.append("relu")
+    x, q53, q87 = r["q"]
+    if not (np.array_equal(orc.quantize_f32(x, 5, 3, L=L), q53)
+            and np.array_equal(orc.quantize_f32(x, 8, 7, L=L), q87)):
+        bad.append("quantize")
+    ifm, w, want, want_relu = r["conv"]
+    if not np.array_equal(orc.conv2d(ifm, w, 1, 1, 5, 3, 4, 4, L=L), want):
+        bad.append("conv")
+    if not np.array_equal(orc.conv2d(ifm, w, 1, 1, 5, 3, 4, 4, act=1, L=L), want_relu):
+        bad.append("conv_relu")
+    return bad
+
+
+def test_unmodified_oracle_passes_reduced_pins(tmp_path, refs):
+    assert failures(compile_variant(tmp_path, "orig", SRC), refs) == []
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(tmp_path, refs, name):
+    old, new = MUTANTS[name]
+    assert SRC.count(old) == 1, f"mutation site for {name} not unique"
+    L = compile_variant(tmp_path, name, SRC.replace(old, new))
+    assert failures(L, refs), f"mutant {name} passed every pin"
