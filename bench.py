@@ -1,0 +1,201 @@
+#!/usr/bin/env python3
+"""Benchmark of the HOBFLOPS MCMK convolution on one MI355X.
+
+Workload: the ResNet-shaped layer 8x56x56x64 -> 64 kernels 3x3, stride 1,
+pad 1, inputs rounded to the 9-bit format (wE, wF) = (5, 3), multiply and
+accumulate in (5, 4) (the paper's HOBFLOPS9 MAC), fixed accumulation order
+(ky, kx, c). One step is the whole path on one batch: quantise + pack the
+float32 IFM and weights into bit-planes, the bitsliced convolution, and
+unpack of the OFM to float32. Inputs are synthetic, seeded, resident in HBM
+before timing starts.
+
+Prints one JSON line: GMAC/s of the step, the convolution kernel against the
+VALU roofline (achieved 32-bit bitwise VALU lane-ops/s from the generated
+netlist's instruction count and the kernel's HIP-event time), and the CPU
+oracle timed on a bounded sample of the same outputs.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2007_06563_amd import hobflops as hf  # noqa: E402
+from paper_2007_06563_amd import inputs as I     # noqa: E402
+
+# MI355X: 256 CUs, 4 SIMDs of 16 lanes each (64 lanes/clk/CU for 32-bit VALU
+# ops), 2.4 GHz peak engine clock.
+N_CU, LANES_PER_CU_CLK, CLOCK_HZ = 256, 64, 2.4e9
+PEAK_LANE_OPS = N_CU * LANES_PER_CU_CLK * CLOCK_HZ   # 3.93e13 32-bit VALU ops/s
+N_SIMD = N_CU * 4
+HBM_PEAK = 8.0e12
+
+IN_FMT, ACC_FMT, OUT_FMT = (5, 3), (5, 4), (5, 4)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(ifm, w, s, gpu_codes, seconds):
+    """The oracle on a bounded random sample of the layer's outputs, all host
+    threads; also its output compared with the GPU's at those points."""
+    import oracle
+    t = time.perf_counter()
+    qi = oracle.quantize_f32(ifm, *IN_FMT)
+    qw = oracle.quantize_f32(w, *IN_FMT)
+    log(f"cpu_baseline: quantised inputs in {time.perf_counter() - t:.1f}s")
+    g = np.random.default_rng(2024)
+    threads = oracle.default_threads()
+    taps = s.KH * s.KW * s.C
+
+    def pts_of(n):
+        return np.stack([g.integers(0, s.N, n), g.integers(0, s.OH, n), g.integers(0, s.OW, n),
+                         g.integers(0, s.M, n)], 1).astype(np.int64)
+
+    probe = pts_of(max(64, threads * 8))
+    t = time.perf_counter()
+    oracle.conv2d_points(qi, qw, probe, s.stride, s.pad, IN_FMT[0], IN_FMT[1], ACC_FMT[1],
+                         OUT_FMT[1], nthreads=threads)
+    rate = len(probe) / max(time.perf_counter() - t, 1e-6)
+    npts = int(min(max(rate * seconds, 256), s.N * s.OH * s.OW * s.M))
+    pts = pts_of(npts)
+    t = time.perf_counter()
+    out = oracle.conv2d_points(qi, qw, pts, s.stride, s.pad, IN_FMT[0], IN_FMT[1], ACC_FMT[1],
+                               OUT_FMT[1], nthreads=threads)
+    dt = time.perf_counter() - t
+    mism = int(np.count_nonzero(out != gpu_codes[pts[:, 0], pts[:, 1], pts[:, 2], pts[:, 3]]))
+    # one thread, smaller sample, for comparison with single-core figures
+    p1 = pts_of(max(32, npts // threads // 4))
+    t = time.perf_counter()
+    oracle.conv2d_points(qi, qw, p1, s.stride, s.pad, IN_FMT[0], IN_FMT[1], ACC_FMT[1],
+                         OUT_FMT[1], nthreads=1)
+    dt1 = time.perf_counter() - t
+    cpu = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {
+        "value": npts * taps / dt / 1e9, "unit": "GMAC/s", "cores": threads, "kind": "oracle",
+        "sample": f"{npts} random outputs of {s.N * s.OH * s.OW * s.M} ({npts * taps} MACs) of "
+                  f"the same layer, {threads} threads over outputs, {dt:.1f}s",
+        "value_1thread": len(p1) * taps / dt1 / 1e9, "cpu_model": cpu,
+        "parity_sample_mismatches": mism, "parity_sample_points": npts,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the layer shards "
+              "by batch with no exchange, so a multi-GPU figure is the single-GPU one times N "
+              "minus launch skew; no multi-GPU path is built.", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.init()
+    dev = torch.device("cuda:0")
+    s = I.RESNET_CONV_SHAPE
+    ifm, w = I.resnet_conv_inputs()
+    d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, IN_FMT, ACC_FMT,
+                     OUT_FMT, hf.ACT_NONE)
+    P = s.N * s.OH * s.OW
+    x_ifm = torch.from_numpy(ifm.reshape(s.N * s.H * s.W, s.C)).to(dev)
+    x_w = torch.from_numpy(w.reshape(s.KH * s.KW * s.C, s.M)).to(dev)
+    p_ifm = torch.empty(hf.plane_shape(s.N * s.H * s.W, s.C, IN_FMT), dtype=torch.int32, device=dev)
+    p_w = torch.empty(hf.plane_shape(s.KH * s.KW * s.C, s.M, IN_FMT), dtype=torch.int32, device=dev)
+    p_ofm = torch.empty(hf.plane_shape(P, s.M, OUT_FMT), dtype=torch.int32, device=dev)
+    y = torch.empty((P, s.M), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev:
+            ev[0].record(stream)
+        hf.pack(x_ifm, IN_FMT, out=p_ifm)
+        hf.pack(x_w, IN_FMT, out=p_w)
+        if ev:
+            ev[1].record(stream)
+        hf.conv2d(p_ifm, p_w, d, out=p_ofm)
+        if ev:
+            ev[2].record(stream)
+        hf.unpack(p_ofm, P, s.M, OUT_FMT, kind="f32", out=y)
+        if ev:
+            ev[3].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    pack_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    conv_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    unpack_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+
+    macs = s.macs
+    G, _ = hf.netlist_ops(IN_FMT, ACC_FMT)
+    lane_ops = macs / 32.0 * G          # 32 MACs per 32-bit word operation
+    achieved = lane_ops / (conv_ms * 1e-3)
+    waves = ((P + 63) // 64) * ((s.M + 31) // 32)
+    pack_bytes = (s.N * s.H * s.W * s.C + s.KH * s.KW * s.C * s.M) * 4 + \
+        (p_ifm.numel() + p_w.numel()) * 4
+    unpack_bytes = p_ofm.numel() * 4 + P * s.M * 4
+    codes = hf.unpack(p_ofm, P, s.M, OUT_FMT, kind="code")
+    torch.cuda.synchronize()
+    gpu_codes = codes.cpu().numpy().view(np.uint32).astype(np.uint64).reshape(s.N, s.OH, s.OW, s.M)
+
+    res = {
+        "metric": "custom-FP conv GMAC/s and % of peak VALU bitwise-op rate, 9-bit fmt",
+        "value": macs / (ms_step * 1e-3) / 1e9,
+        "unit": "GMAC/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "e5m3 in, e5m4 acc, bitsliced on u32 planes",
+        "data": "synthetic (seeded): IFM |N(0,1)| half zeroed, weights N(0,0.05)",
+        "config": {"workload": "MCMK conv 8x56x56x64 -> 64 kernels 3x3, stride 1, pad 1, "
+                               "HOBFLOPS9 (5,3)->(5,4), order (ky,kx,c); step = pack IFM and "
+                               "weights + conv + unpack OFM",
+                   "macs_per_step": macs, "batch": s.N},
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
+                     "unit": "T VALU-op/s (32-bit bitwise, one op = 32 gates)",
+                     "frac": achieved / PEAK_LANE_OPS, "traffic": None,
+                     "kernel": "conv2d_kernel", "ops_per_mac_word": G,
+                     "kernel_ms": conv_ms, "wave_ceiling": min(1.0, waves / N_SIMD)},
+        "pct_valu_peak": 100.0 * achieved / PEAK_LANE_OPS,
+        "conv_gmacs": macs / (conv_ms * 1e-3) / 1e9,
+        "pack_ms": pack_ms, "unpack_ms": unpack_ms,
+        "pack_gbps": pack_bytes / (pack_ms * 1e-3) / 1e9,
+        "unpack_gbps": unpack_bytes / (unpack_ms * 1e-3) / 1e9,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(ifm, w, s, gpu_codes, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

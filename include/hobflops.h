@@ -1,0 +1,133 @@
+/*
+ * hobflops.h -- C ABI of libhobflops.so: bitsliced custom-precision
+ * floating-point (HOBFLOPS) arithmetic and MCMK convolution on MI355X (gfx950).
+ *
+ * Number format (paper Sec. 3.3): a FloPoCo word of NB = 3 + wE + wF bits,
+ * held LSB first in a code: fraction F in bits [0, wF), exponent E in
+ * [wF, wF+wE), sign at wF+wE, 2-bit exception field above it (00 zero,
+ * 01 normal, 10 infinity, 11 NaN). Exponent bias 2^(wE-1) - 1; no subnormal
+ * numbers; every E is an ordinary binade. Every operation rounds to nearest,
+ * ties to even (paper Sec. 4), with an unbounded exponent first and the range
+ * check after: overflow gives a signed infinity, underflow a zero with the sign
+ * of the exact value. NaN, infinity and zero signs follow IEEE-754. Results are
+ * canonical: E = F = 0 for zero and infinity, s = E = F = 0 for NaN.
+ *
+ * Plane layout PL32 (bitslice-parallel layout of paper Sec. 3.2): a tensor of
+ * logical shape [rows][len], packed along len, is stored as uint32
+ * words[rows][ceil(len/32)][NB]; bit j of words[r][g][b] is bit b of the code
+ * of element (r, 32*g + j). Lanes past len hold code 0 (+0).
+ *
+ * Conventions for every entry point:
+ *  - Pointers are device pointers (HBM) owned by the caller; the library
+ *    allocates no device memory. Inputs and outputs of one call must not
+ *    overlap. Pointers must be 4-byte aligned.
+ *  - `stream` is a hipStream_t (NULL = the default stream). Calls enqueue work
+ *    on it and return without synchronising.
+ *  - Arguments are checked before anything is launched; a rejected call
+ *    launches nothing and returns a negative status (see below).
+ *  - Supported widths: 2 <= wE <= 8, 1 <= wF <= 23, NB <= 32. The convolution
+ *    and element-wise MAC run only for the format combinations the library was
+ *    generated for (hobflops_conv2d_supported / hobflops_muladd_supported);
+ *    other combinations return HOBFLOPS_EUNSUPPORTED.
+ *  - The library keeps no state between calls and is safe to call from
+ *    several host threads.
+ */
+#ifndef HOBFLOPS_H
+#define HOBFLOPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+  int wE; /* exponent bits */
+  int wF; /* fraction bits */
+} hobflops_fmt;
+
+enum {
+  HOBFLOPS_OK = 0,
+  HOBFLOPS_EINVAL = -1,       /* bad size, shape, format or null pointer */
+  HOBFLOPS_EUNSUPPORTED = -2, /* valid request, no generated kernel for it */
+  HOBFLOPS_EALIGN = -3,       /* a pointer is not 4-byte aligned */
+  HOBFLOPS_EHIP = -4          /* the HIP runtime reported an error */
+};
+
+enum { HOBFLOPS_SRC_F32 = 0, HOBFLOPS_SRC_CODE_U32 = 1 };
+enum { HOBFLOPS_ROUND_NEAREST_EVEN = 0 };
+enum { HOBFLOPS_ORDER_KY_KX_C = 0 };
+enum { HOBFLOPS_ACT_NONE = 0, HOBFLOPS_ACT_RELU = 1 };
+
+/* Number of uint32 words of a PL32 tensor: rows * ceil(len/32) * NB.
+ * Returns HOBFLOPS_OK and writes *words, or HOBFLOPS_EINVAL. */
+int hobflops_plane_words(int64_t rows, int64_t len, hobflops_fmt f, int64_t* words);
+
+/* Quantise and pack (paper Sec. 3.4 and the convolution figure: data are
+ * transformed to the bitslice layout before the first layer).
+ * src: rows*len elements, row-major; kind HOBFLOPS_SRC_F32 = float32 values,
+ * each rounded to format f (the exact float32 value, subnormals included;
+ * NaN -> NaN, +-inf -> +-inf, +-0 -> +-0); kind HOBFLOPS_SRC_CODE_U32 = codes
+ * in format f (bits above NB ignored; fields of non-normal codes are kept as
+ * given). planes: hobflops_plane_words(rows, len, f) words, fully written. */
+int hobflops_pack(const void* src, int kind, int64_t rows, int64_t len, hobflops_fmt f,
+                  uint32_t* planes, void* stream);
+
+/* Unpack (paper Sec. 3.4: transformed back to floats after the last layer).
+ * planes: PL32 tensor of format f; dst: rows*len elements, row-major; kind
+ * HOBFLOPS_SRC_CODE_U32 writes codes (bits above NB zero), HOBFLOPS_SRC_F32
+ * writes float32: the exact value rounded to nearest even float32 (exact for
+ * wE <= 7), NaN as 0x7FC00000. */
+int hobflops_unpack(const uint32_t* planes, int64_t rows, int64_t len, hobflops_fmt f, int kind,
+                    void* dst, void* stream);
+
+/* Multi-channel multi-kernel convolution whose every multiply-add is a
+ * bitsliced custom-precision multiply followed by an add (paper Sec. 3.4).
+ *   ifm: PL32, rows N*H*W (NHWC order), len C, format in_fmt
+ *   w:   PL32, rows KH*KW*C (HWIO order, row (ky*KW + kx)*C + c), len M, in_fmt
+ *   ofm: PL32, rows N*OH*OW, len M, format out_fmt; OH = (H + 2*pad - KH)/stride + 1
+ * For each output (n, oy, ox, m): acc = +0 in acc_fmt; for ky, then kx, then c:
+ *   acc = add(acc, mul(w[ky][kx][c][m], x)), x the IFM value or +0 for a
+ *   padding tap, mul rounding into acc_fmt and add rounding in acc_fmt; then
+ *   ofm = convert(act(acc)) into out_fmt (ReLU: NaN stays NaN, negatives and -0
+ *   give +0). All formats share wE; acc_fmt.wF >= in_fmt.wF.
+ *   round must be HOBFLOPS_ROUND_NEAREST_EVEN, order HOBFLOPS_ORDER_KY_KX_C. */
+typedef struct {
+  int N, H, W, C, M, KH, KW, stride, pad;
+  hobflops_fmt in_fmt, acc_fmt, out_fmt;
+  int act, round, order;
+} hobflops_conv_desc;
+
+int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
+                    const hobflops_conv_desc* d, void* stream);
+
+/* 1 if hobflops_conv2d has a kernel for d's formats and activation, else 0. */
+int hobflops_conv2d_supported(const hobflops_conv_desc* d);
+
+/* Element-wise r = add(widen(c), mul(a, b)) over n elements of flat PL32
+ * tensors (rows 1, len n): a, b, c in in_fmt, r in acc_fmt (same wE,
+ * acc_fmt.wF >= in_fmt.wF); the product is rounded into acc_fmt, c widened
+ * exactly, the sum rounded once more (the paper's MAC: a multiplier then an
+ * adder, Sec. 3.3 and Table 3). */
+int hobflops_muladd(const uint32_t* a, const uint32_t* b, const uint32_t* c, uint32_t* r,
+                    int64_t n, hobflops_fmt in_fmt, hobflops_fmt acc_fmt, void* stream);
+
+int hobflops_muladd_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt);
+
+/* Bitwise VALU instructions per 32-lane word in the generated netlists of a
+ * MAC (in_fmt x in_fmt -> acc_fmt, then acc_fmt + acc_fmt): the convolution's
+ * fused step, and the element-wise kernel's (the paper's gate count,
+ * Sec. 4: throughput follows it). Returns HOBFLOPS_OK or
+ * HOBFLOPS_EUNSUPPORTED; any output pointer may be NULL. */
+int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int* conv_mac_ops,
+                         int* muladd_ops);
+
+/* Text for a status code; for HOBFLOPS_EHIP, the last HIP error of this
+ * thread. The pointer stays valid until the next call on the same thread. */
+const char* hobflops_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

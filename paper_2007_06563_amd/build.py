@@ -1,0 +1,212 @@
+"""Build libhobflops.so: generate the netlists, emit HIP, compile for gfx950.
+
+Steps (the paper's flow, Sec. 3 and its flow figure, with this package's own
+tools): build each operator circuit (gen.fp), optimise it and map it onto
+3-input LUT cells (gen.opt), emit it as straight-line HIP (gen.emit), then
+compile every kernel variant with hipcc for gfx950 and link one shared library
+next to this file. Generated sources go to _gen/ (not part of the source tree).
+"""
+import concurrent.futures as cf
+import hashlib
+import json
+import os
+import shutil
+import subprocess
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+GEN = os.path.join(HERE, "_gen")
+OBJ = os.path.join(HERE, "_build")
+LIB = os.path.join(HERE, "libhobflops.so")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+HIPFLAGS = ["-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC",
+            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            "-I", os.path.join(ROOT, "include"), "-I", os.path.join(HERE, "csrc"), "-I", GEN]
+
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2007_06563_amd import variants  # noqa: E402
+from paper_2007_06563_amd.gen import emit, fp, opt  # noqa: E402
+
+
+def nb(wE, wF):
+    return 3 + wE + wF
+
+
+def _gen_sources_digest():
+    h = hashlib.sha256()
+    for name in ("circuit.py", "fp.py", "opt.py", "emit.py"):
+        h.update(open(os.path.join(HERE, "gen", name), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def netlist(kind, key, cache):
+    """Optimised circuit for one operator; cached per generator version."""
+    name = {"mac": "mac_e{}m{}_a{}", "epi": "epi_e{}m{}_o{}{}", "muladd": "muladd_e{}m{}_a{}"}[kind]
+    if kind == "epi":
+        wE, wa, wo, act = key
+        fname = name.format(wE, wa, wo, "_relu" if act else "")
+    else:
+        fname = name.format(*key)
+    if fname in cache:
+        return fname, cache[fname]
+    if kind == "mac":
+        C = fp.mac_circuit(*key)
+        text_kw = {"in_place": "acc"}
+    elif kind == "epi":
+        wE, wa, wo, act = key
+        C = fp.convert_circuit(wE, wa, wo, relu=bool(act), canonical=True)
+        text_kw = {}
+    else:
+        C = fp.muladd_circuit(*key)
+        text_kw = {}
+    raw = C.n_nodes()
+    C = opt.optimize(C)
+    entry = {"text": emit.emit_function(C, fname, **text_kw), "ops": emit.op_count(C),
+             "raw_nodes": raw}
+    cache[fname] = entry
+    return fname, entry
+
+
+def generate(verbose=True):
+    os.makedirs(GEN, exist_ok=True)
+    digest = _gen_sources_digest()
+    cache_path = os.path.join(GEN, "netlists.json")
+    cache = {}
+    if os.path.exists(cache_path):
+        data = json.load(open(cache_path))
+        if data.get("digest") == digest:
+            cache = data["netlists"]
+    files = []
+    reg_conv, reg_mul = [], []
+    for v in variants.CONV_VARIANTS:
+        wE, wi, wa, wo, act = v
+        tag = variants.conv_tag(v)
+        mac, mac_e = netlist("mac", (wE, wi, wa), cache)
+        epi, _ = netlist("epi", (wE, wa, wo, act), cache)
+        src = f"""// Generated: convolution variant {tag}. Do not edit.
+#include "kernels.hpp"
+#include "registry.hpp"
+namespace hobflops {{
+namespace conv_{tag} {{
+{cache[mac]['text']}
+{cache[epi]['text']}
+struct V {{
+  static constexpr int NIN = {nb(wE, wi)}, NACC = {nb(wE, wa)}, NOUT = {nb(wE, wo)};
+  static __device__ __forceinline__ void mac(uint32_t (&acc)[NACC], const uint32_t (&w)[NIN],
+                                             const uint32_t (&x)[NIN]) {{ {mac}(acc, w, x); }}
+  static __device__ __forceinline__ void epi(const uint32_t (&acc)[NACC], uint32_t (&out)[NOUT]) {{
+    {epi}(acc, out);
+  }}
+}};
+}}  // namespace conv_{tag}
+hipError_t launch_conv_{tag}(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
+                              const ConvParams& p, hipStream_t stream) {{
+  dim3 grid((unsigned)((p.P + kConvBlock - 1) / kConvBlock), (unsigned)p.MT);
+  hipLaunchKernelGGL(conv2d_kernel<conv_{tag}::V>, grid, dim3(kConvBlock), 0, stream, ifm, w, ofm, p);
+  return hipGetLastError();
+}}
+}}  // namespace hobflops
+"""
+        files.append((f"conv_{tag}.hip", src))
+        reg_conv.append((v, tag, mac_e["ops"]))
+    for v in variants.MULADD_VARIANTS:
+        wE, wi, wa = v
+        tag = variants.muladd_tag(v)
+        fn, e = netlist("muladd", (wE, wi, wa), cache)
+        src = f"""// Generated: element-wise MAC variant {tag}. Do not edit.
+#include "kernels.hpp"
+#include "registry.hpp"
+namespace hobflops {{
+namespace muladd_{tag} {{
+{cache[fn]['text']}
+struct V {{
+  static constexpr int NIN = {nb(wE, wi)}, NACC = {nb(wE, wa)};
+  static __device__ __forceinline__ void muladd(const uint32_t (&a)[NIN], const uint32_t (&b)[NIN],
+                                                const uint32_t (&c)[NIN], uint32_t (&r)[NACC]) {{
+    {fn}(a, b, c, r);
+  }}
+}};
+}}  // namespace muladd_{tag}
+hipError_t launch_muladd_{tag}(const uint32_t* a, const uint32_t* b, const uint32_t* c,
+                                uint32_t* r, int64_t groups, hipStream_t stream) {{
+  const unsigned blocks = (unsigned)((groups + 255) / 256);
+  hipLaunchKernelGGL(muladd_kernel<muladd_{tag}::V>, dim3(blocks), dim3(256), 0, stream, a, b, c, r, groups);
+  return hipGetLastError();
+}}
+}}  // namespace hobflops
+"""
+        files.append((f"muladd_{tag}.hip", src))
+        reg_mul.append((v, tag, e["ops"]))
+    reg = ["// Generated: table of kernel variants (host code). Do not edit.",
+           '#include "registry.hpp"', "#ifndef __HIP_DEVICE_COMPILE__", "namespace hobflops {"]
+    for v, tag, ops in reg_conv:
+        reg.append(f"hipError_t launch_conv_{tag}(const uint32_t*, const uint32_t*, uint32_t*, "
+                   f"const ConvParams&, hipStream_t);")
+    for v, tag, ops in reg_mul:
+        reg.append(f"hipError_t launch_muladd_{tag}(const uint32_t*, const uint32_t*, const uint32_t*, "
+                   f"uint32_t*, int64_t, hipStream_t);")
+    reg.append("const ConvVariant kConvVariants[] = {")
+    for v, tag, ops in reg_conv:
+        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {v[4]}, {ops}, launch_conv_{tag}}},")
+    reg.append("};")
+    reg.append(f"const int kNumConvVariants = {len(reg_conv)};")
+    reg.append("const MuladdVariant kMuladdVariants[] = {")
+    for v, tag, ops in reg_mul:
+        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {ops}, launch_muladd_{tag}}},")
+    reg.append("};")
+    reg.append(f"const int kNumMuladdVariants = {len(reg_mul)};")
+    reg.append("}  // namespace hobflops")
+    reg.append("#endif")
+    files.append(("registry.hip", "\n".join(reg) + "\n"))
+    for name, text in files:
+        path = os.path.join(GEN, name)
+        if not os.path.exists(path) or open(path).read() != text:
+            with open(path, "w") as f:
+                f.write(text)
+    json.dump({"digest": digest, "netlists": cache}, open(cache_path, "w"))
+    gates = {k: {"ops": e["ops"], "raw_nodes": e["raw_nodes"]} for k, e in cache.items()}
+    json.dump(gates, open(os.path.join(GEN, "gates.json"), "w"), indent=1, sort_keys=True)
+    if verbose:
+        for k in sorted(gates):
+            print(f"  {k}: {gates[k]['ops']} ops (raw {gates[k]['raw_nodes']})")
+    return [os.path.join(GEN, n) for n, _ in files]
+
+
+def _compile(src, obj):
+    cmd = [HIPCC] + HIPFLAGS + ["-c", src, "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr[-4000:]}")
+    return obj
+
+
+def build(jobs=None, verbose=True):
+    """Generate and compile everything; returns the library path."""
+    gen_files = generate(verbose=verbose)
+    srcs = [os.path.join(HERE, "csrc", "abi.hip"), os.path.join(HERE, "csrc", "pack.hip")] + gen_files
+    os.makedirs(OBJ, exist_ok=True)
+    jobs = jobs or min(16, os.cpu_count() or 4)
+    objs = []
+    with cf.ThreadPoolExecutor(jobs) as ex:
+        futs = []
+        for s in srcs:
+            o = os.path.join(OBJ, os.path.basename(s) + ".o")
+            futs.append(ex.submit(_compile, s, o))
+        for f in futs:
+            objs.append(f.result())
+    tmp = LIB + ".tmp"
+    cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp] + objs
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stderr[-4000:]}")
+    os.replace(tmp, LIB)
+    if verbose:
+        print("built", LIB)
+    return LIB
+
+
+if __name__ == "__main__":
+    build()

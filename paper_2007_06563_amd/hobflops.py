@@ -1,0 +1,186 @@
+"""Python binding of libhobflops.so (ctypes).
+
+Argument marshalling only: every step runs in the library's HIP kernels, on
+torch's current stream; torch supplies device memory and streams. There is no
+CPU fallback: a missing library or a host tensor raises.
+Plane tensors are int32 (the bit patterns of PL32 words).
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libhobflops.so")
+_lib = None
+
+SRC_F32, SRC_CODE_U32 = 0, 1
+ACT_NONE, ACT_RELU = 0, 1
+ROUND_NEAREST_EVEN, ORDER_KY_KX_C = 0, 0
+
+
+class HobflopsError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"hobflops status {status}: {msg}")
+        self.status = status
+
+
+class Fmt(ctypes.Structure):
+    _fields_ = [("wE", ctypes.c_int), ("wF", ctypes.c_int)]
+
+    def __repr__(self):
+        return f"Fmt({self.wE}, {self.wF})"
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int), ("H", ctypes.c_int), ("W", ctypes.c_int),
+                ("C", ctypes.c_int), ("M", ctypes.c_int), ("KH", ctypes.c_int),
+                ("KW", ctypes.c_int), ("stride", ctypes.c_int), ("pad", ctypes.c_int),
+                ("in_fmt", Fmt), ("acc_fmt", Fmt), ("out_fmt", Fmt),
+                ("act", ctypes.c_int), ("round", ctypes.c_int), ("order", ctypes.c_int)]
+
+
+EXPORTS = ("hobflops_plane_words", "hobflops_pack", "hobflops_unpack", "hobflops_conv2d",
+           "hobflops_conv2d_supported", "hobflops_muladd", "hobflops_muladd_supported",
+           "hobflops_netlist_ops", "hobflops_status_string")
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2007_06563_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+        L.hobflops_plane_words.argtypes = [i64, i64, Fmt, ctypes.POINTER(i64)]
+        L.hobflops_pack.argtypes = [vp, ci, i64, i64, Fmt, vp, vp]
+        L.hobflops_unpack.argtypes = [vp, i64, i64, Fmt, ci, vp, vp]
+        L.hobflops_conv2d.argtypes = [vp, vp, vp, ctypes.POINTER(ConvDesc), vp]
+        L.hobflops_conv2d_supported.argtypes = [ctypes.POINTER(ConvDesc)]
+        L.hobflops_muladd.argtypes = [vp, vp, vp, vp, i64, Fmt, Fmt, vp]
+        L.hobflops_muladd_supported.argtypes = [Fmt, Fmt]
+        L.hobflops_netlist_ops.argtypes = [Fmt, Fmt, ctypes.POINTER(ci), ctypes.POINTER(ci)]
+        L.hobflops_status_string.argtypes = [ci]
+        L.hobflops_status_string.restype = ctypes.c_char_p
+        for name in EXPORTS[:-1]:
+            getattr(L, name).restype = ci
+        _lib = L
+    return _lib
+
+
+def fmt(f):
+    return f if isinstance(f, Fmt) else Fmt(int(f[0]), int(f[1]))
+
+
+def nb(f):
+    f = fmt(f)
+    return 3 + f.wE + f.wF
+
+
+def _check(rc):
+    if rc != 0:
+        raise HobflopsError(rc, lib().hobflops_status_string(rc).decode())
+
+
+def _ptr(t):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError("hobflops operates on GPU tensors only")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(t):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def plane_words(rows, length, f):
+    w = ctypes.c_int64()
+    _check(lib().hobflops_plane_words(rows, length, fmt(f), ctypes.byref(w)))
+    return w.value
+
+
+def plane_shape(rows, length, f):
+    return (rows, (length + 31) // 32, nb(f))
+
+
+def pack(src, f, rows=None, length=None, out=None):
+    """float32 values or int32 codes [rows, length] (any shape whose last axis
+    is the packed one) -> int32 planes [rows, ceil(length/32), NB]."""
+    f = fmt(f)
+    if length is None:
+        length = src.shape[-1]
+    if rows is None:
+        rows = src.numel() // max(length, 1)
+    if src.numel() != rows * length:
+        raise ValueError("rows * length does not match the source size")
+    if src.dtype == torch.float32:
+        kind = SRC_F32
+    elif src.dtype in (torch.int32, torch.uint32):
+        kind = SRC_CODE_U32
+    else:
+        raise TypeError("pack takes float32 values or int32 codes")
+    if out is None:
+        out = torch.empty(plane_shape(rows, length, f), dtype=torch.int32, device=src.device)
+    _check(lib().hobflops_pack(_ptr(src), kind, rows, length, f, _ptr(out), _stream(src)))
+    return out
+
+
+def unpack(planes, rows, length, f, kind="f32", out=None):
+    """int32 planes -> float32 values (kind 'f32') or int32 codes ('code'), [rows, length]."""
+    f = fmt(f)
+    k = SRC_F32 if kind == "f32" else SRC_CODE_U32
+    if out is None:
+        out = torch.empty((rows, length), dtype=torch.float32 if k == SRC_F32 else torch.int32,
+                          device=planes.device)
+    _check(lib().hobflops_unpack(_ptr(planes), rows, length, f, k, _ptr(out), _stream(planes)))
+    return out
+
+
+def conv_desc(N, H, W, C, M, KH, KW, stride, pad, in_fmt, acc_fmt, out_fmt, act=ACT_NONE):
+    return ConvDesc(N, H, W, C, M, KH, KW, stride, pad, fmt(in_fmt), fmt(acc_fmt), fmt(out_fmt),
+                    act, ROUND_NEAREST_EVEN, ORDER_KY_KX_C)
+
+
+def conv_out_hw(d):
+    return ((d.H + 2 * d.pad - d.KH) // d.stride + 1, (d.W + 2 * d.pad - d.KW) // d.stride + 1)
+
+
+def conv2d(ifm, w, d, out=None):
+    """ifm planes [N*H*W, ceil(C/32), NB_in], w planes [KH*KW*C, ceil(M/32), NB_in]
+    -> ofm planes [N*OH*OW, ceil(M/32), NB_out]."""
+    OH, OW = conv_out_hw(d)
+    if out is None:
+        out = torch.empty(plane_shape(d.N * OH * OW, d.M, d.out_fmt), dtype=torch.int32,
+                          device=ifm.device)
+    _check(lib().hobflops_conv2d(_ptr(ifm), _ptr(w), _ptr(out), ctypes.byref(d), _stream(ifm)))
+    return out
+
+
+def conv2d_supported(d):
+    return bool(lib().hobflops_conv2d_supported(ctypes.byref(d)))
+
+
+def muladd(a, b, c, n, in_fmt, acc_fmt, out=None):
+    """Element-wise add(widen(c), mul(a, b)) on flat planes of n elements."""
+    in_fmt, acc_fmt = fmt(in_fmt), fmt(acc_fmt)
+    if out is None:
+        out = torch.empty(plane_shape(1, n, acc_fmt), dtype=torch.int32, device=a.device)
+    _check(lib().hobflops_muladd(_ptr(a), _ptr(b), _ptr(c), _ptr(out), n, in_fmt, acc_fmt,
+                                 _stream(a)))
+    return out
+
+
+def muladd_supported(in_fmt, acc_fmt):
+    return bool(lib().hobflops_muladd_supported(fmt(in_fmt), fmt(acc_fmt)))
+
+
+def netlist_ops(in_fmt, acc_fmt):
+    """(conv MAC ops, element-wise MAC ops) per 32-lane word; 0 where not generated."""
+    a, b = ctypes.c_int(), ctypes.c_int()
+    rc = lib().hobflops_netlist_ops(fmt(in_fmt), fmt(acc_fmt), ctypes.byref(a), ctypes.byref(b))
+    if rc != 0:
+        raise HobflopsError(rc, lib().hobflops_status_string(rc).decode())
+    return a.value, b.value

@@ -1,0 +1,125 @@
+"""The C ABI on the host: the library loads, exports every function the header
+declares, and rejects bad arguments before launching anything (CPU only --
+none of these calls reaches the GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def hf():
+    from paper_2007_06563_amd import hobflops
+    if not os.path.exists(hobflops.LIB_PATH):
+        from paper_2007_06563_amd import build
+        build.build(verbose=False)
+    hobflops.lib()
+    return hobflops
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "hobflops.h")).read()
+    return sorted(set(re.findall(r"\b(hobflops_\w+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(hf):
+    names = declared_functions()
+    assert len(names) >= 9
+    L = hf.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(hf.EXPORTS)
+
+
+def test_plane_words(hf):
+    assert hf.plane_words(10, 64, (5, 3)) == 10 * 2 * 11
+    assert hf.plane_words(3, 33, (5, 4)) == 3 * 2 * 12
+    assert hf.plane_words(0, 5, (5, 3)) == 0
+    with pytest.raises(hf.HobflopsError):
+        hf.plane_words(-1, 5, (5, 3))
+    with pytest.raises(hf.HobflopsError):
+        hf.plane_words(1, 5, (9, 3))
+
+
+FAKE = ctypes.c_void_p(0x10000)      # never dereferenced: calls fail before launch
+MISALIGNED = ctypes.c_void_p(0x10002)
+
+
+def desc(hf, **kw):
+    base = dict(N=1, H=8, W=8, C=4, M=8, KH=3, KW=3, stride=1, pad=1, in_fmt=(5, 3),
+                acc_fmt=(5, 4), out_fmt=(5, 4), act=0)
+    base.update(kw)
+    return hf.conv_desc(**base)
+
+
+@pytest.mark.parametrize("bad", [dict(N=0), dict(C=-1), dict(stride=0), dict(pad=-1),
+                                 dict(KH=11), dict(acc_fmt=(4, 4)), dict(acc_fmt=(5, 2)),
+                                 dict(in_fmt=(1, 3)), dict(out_fmt=(5, 30)), dict(act=7)])
+def test_conv_rejects_bad_descriptors(hf, bad):
+    d = desc(hf, **bad)
+    assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -1
+    assert not hf.conv2d_supported(d)
+
+
+def test_conv_rejects_round_and_order(hf):
+    d = desc(hf)
+    d.round = 1
+    assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -1
+    d = desc(hf)
+    d.order = 2
+    assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -1
+
+
+def test_conv_null_misaligned_unsupported(hf):
+    L = hf.lib()
+    d = desc(hf)
+    assert L.hobflops_conv2d(None, FAKE, FAKE, ctypes.byref(d), None) == -1
+    assert L.hobflops_conv2d(FAKE, MISALIGNED, FAKE, ctypes.byref(d), None) == -3
+    assert L.hobflops_conv2d(FAKE, FAKE, FAKE, None, None) == -1
+    u = desc(hf, in_fmt=(5, 3), acc_fmt=(5, 9), out_fmt=(5, 9))
+    assert not hf.conv2d_supported(u)
+    assert L.hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(u), None) == -2
+    assert hf.conv2d_supported(desc(hf))
+
+
+def test_pack_unpack_argument_checks(hf):
+    L = hf.lib()
+    f = hf.Fmt(5, 3)
+    assert L.hobflops_pack(FAKE, 0, 4, 40, hf.Fmt(5, 40), FAKE, None) == -1
+    assert L.hobflops_pack(FAKE, 5, 4, 40, f, FAKE, None) == -1
+    assert L.hobflops_pack(None, 0, 4, 40, f, FAKE, None) == -1
+    assert L.hobflops_pack(MISALIGNED, 0, 4, 40, f, FAKE, None) == -3
+    assert L.hobflops_pack(None, 0, 0, 40, f, None, None) == 0  # empty: nothing to do
+    assert L.hobflops_unpack(FAKE, -1, 40, f, 0, FAKE, None) == -1
+    assert L.hobflops_unpack(FAKE, 4, 40, f, 0, MISALIGNED, None) == -3
+
+
+def test_muladd_argument_checks(hf):
+    L = hf.lib()
+    a = hf.Fmt(5, 3)
+    assert L.hobflops_muladd(FAKE, FAKE, FAKE, FAKE, -5, a, hf.Fmt(5, 4), None) == -1
+    assert L.hobflops_muladd(FAKE, FAKE, FAKE, FAKE, 64, a, hf.Fmt(4, 4), None) == -1
+    assert L.hobflops_muladd(FAKE, FAKE, FAKE, FAKE, 64, a, hf.Fmt(5, 9), None) == -2
+    assert L.hobflops_muladd(FAKE, FAKE, None, FAKE, 64, a, hf.Fmt(5, 4), None) == -1
+    assert L.hobflops_muladd(FAKE, FAKE, FAKE, MISALIGNED, 64, a, hf.Fmt(5, 4), None) == -3
+    assert hf.muladd_supported((5, 3), (5, 4))
+    assert not hf.muladd_supported((5, 3), (5, 9))
+
+
+def test_netlist_ops_and_status_strings(hf):
+    conv_ops, mul_ops = hf.netlist_ops((5, 3), (5, 4))
+    assert 50 < conv_ops < 1000 and 50 < mul_ops < 1000
+    with pytest.raises(hf.HobflopsError):
+        hf.netlist_ops((5, 3), (5, 9))
+    L = hf.lib()
+    for s in (0, -1, -2, -3, -4, 12):
+        assert L.hobflops_status_string(s)
+
+
+def test_python_binding_refuses_host_tensors(hf):
+    import torch
+    with pytest.raises(TypeError):
+        hf.pack(torch.zeros(4, 32), (5, 3))

@@ -1,0 +1,188 @@
+"""GPU parity: the HIP path through the C ABI against the oracle, bit for bit.
+
+Every comparison is of codes (integers): zero mismatches allowed. Inputs are
+seeded; each case prints what it runs before touching the GPU.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from gpu_util import codes_of, dev, need_gpu, say
+from paper_2007_06563_amd import inputs as I
+from paper_2007_06563_amd import variants
+from planes import pack_codes, unpack_planes
+
+pytestmark = pytest.mark.gpu
+
+
+def rand_f32(seed, n, lo=-4.0, hi=4.0, specials=0.02):
+    g = np.random.default_rng([7, seed])
+    x = g.uniform(lo, hi, n).astype(np.float32)
+    # plus raw bit patterns (all exponents, subnormals, NaN payloads)
+    raw = g.integers(0, 1 << 32, n // 4, dtype=np.uint64).astype(np.uint32).view(np.float32)
+    x[: n // 4] = raw
+    return I.inject_specials(x, g, specials)
+
+
+# NB = 3 + wE + wF must fit a 32-bit code: (8,21) and (7,22) are the widest
+PACK_FORMATS = [(2, 1), (4, 2), (4, 3), (5, 2), (5, 3), (5, 4), (5, 10), (5, 11), (8, 7), (8, 8),
+                (8, 21), (7, 22), (6, 12)]
+
+
+@pytest.mark.parametrize("wE,wF", PACK_FORMATS)
+def test_pack_unpack_float32(wE, wF):
+    hf = need_gpu()
+    rows, length = 37, 70  # ragged: 3 groups per row, odd number of groups
+    x = rand_f32(wE * 100 + wF, rows * length).reshape(rows, length)
+    say(f"pack f32 fmt=({wE},{wF}) shape={x.shape}")
+    planes = hf.pack(dev(x), (wE, wF))
+    torch.cuda.synchronize()
+    want = orc.quantize_f32(x, wE, wF)
+    nbits = 3 + wE + wF
+    assert np.array_equal(planes.cpu().numpy().view(np.uint32), pack_codes(want, nbits))
+    codes = hf.unpack(planes, rows, length, (wE, wF), kind="code")
+    vals = hf.unpack(planes, rows, length, (wE, wF), kind="f32")
+    torch.cuda.synchronize()
+    assert np.array_equal(codes_of(codes), want)
+    want_f = orc.decode_f32(want, wE, wF)
+    assert np.array_equal(vals.cpu().numpy().view(np.uint32), want_f.view(np.uint32))
+
+
+@pytest.mark.parametrize("wE,wF", [(5, 3), (5, 4), (8, 8)])
+def test_pack_codes_round_trip(wE, wF):
+    hf = need_gpu()
+    nbits = 3 + wE + wF
+    rows, length = 5, 1000
+    raw = I.random_codes(nbits, (rows, length), 32)  # garbage above NB too
+    say(f"pack codes fmt=({wE},{wF})")
+    planes = hf.pack(dev(raw.view(np.int32)), (wE, wF))
+    back = hf.unpack(planes, rows, length, (wE, wF), kind="code")
+    torch.cuda.synchronize()
+    masked = raw.astype(np.uint64) & np.uint64((1 << nbits) - 1)
+    assert np.array_equal(codes_of(back), masked)
+    assert np.array_equal(unpack_planes(planes.cpu().numpy(), length), masked)
+
+
+def test_wider_than_32_bit_codes_rejected():
+    hf = need_gpu()
+    with pytest.raises(hf.HobflopsError):
+        hf.pack(torch.zeros((2, 32), device="cuda"), (8, 23))
+
+
+def test_empty_pack_is_a_no_op():
+    hf = need_gpu()
+    hf.pack(torch.empty((0, 5), device="cuda"), (5, 3), rows=0, length=5)
+
+
+@pytest.mark.parametrize("v", variants.MULADD_VARIANTS, ids=variants.muladd_tag)
+def test_muladd_vs_oracle(v):
+    hf = need_gpu()
+    wE, wi, wa = v
+    n = (1 << 15) + 77  # ragged tail
+    a, b, c = (rand_f32(1000 * wi + t, n) for t in range(3))
+    say(f"muladd {v} n={n}")
+    pa, pb, pc = (hf.pack(dev(t), (wE, wi)) for t in (a, b, c))
+    r = hf.muladd(pa, pb, pc, n, (wE, wi), (wE, wa))
+    got = codes_of(hf.unpack(r, 1, n, (wE, wa), kind="code"))[0]
+    qa, qb, qc = (orc.quantize_f32(t, wE, wi) for t in (a, b, c))
+    want = orc.muladd(qa, qb, qc, wE, wi, wa)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{bad.size} mismatches; first a={qa[bad[0]]:#x} b={qb[bad[0]]:#x} " \
+                          f"c={qc[bad[0]]:#x} got={got[bad[0]]:#x} want={want[bad[0]]:#x}"
+
+
+@pytest.mark.parametrize("v", variants.MULADD_VARIANTS, ids=variants.muladd_tag)
+def test_muladd_raw_codes_vs_oracle(v):
+    """Non-canonical inputs: every field bit random, specials with garbage fields."""
+    hf = need_gpu()
+    wE, wi, wa = v
+    nbits = 3 + wE + wi
+    n = 1 << 14
+    a, b, c = (I.random_codes(nbits * 10 + t, (1, n), nbits) for t in range(3))
+    say(f"muladd raw codes {v}")
+    pa, pb, pc = (hf.pack(dev(t.view(np.int32)), (wE, wi)) for t in (a, b, c))
+    r = hf.muladd(pa, pb, pc, n, (wE, wi), (wE, wa))
+    got = codes_of(hf.unpack(r, 1, n, (wE, wa), kind="code"))[0]
+    want = orc.muladd(a[0].astype(np.uint64), b[0].astype(np.uint64), c[0].astype(np.uint64), wE,
+                      wi, wa)
+    assert np.array_equal(got, want)
+
+
+def run_conv(hf, ifm_codes, w_codes, stride, pad, wE, wi, wa, wo, act):
+    """GPU conv on code tensors (NHWC / HWIO) -> output codes [N, OH, OW, M]."""
+    N, H, W, C = ifm_codes.shape
+    KH, KW, _, M = w_codes.shape
+    d = hf.conv_desc(N, H, W, C, M, KH, KW, stride, pad, (wE, wi), (wE, wa), (wE, wo), act)
+    OH, OW = hf.conv_out_hw(d)
+    pi = hf.pack(dev(ifm_codes.astype(np.uint32).view(np.int32).reshape(N * H * W, C)), (wE, wi))
+    pw = hf.pack(dev(w_codes.astype(np.uint32).view(np.int32).reshape(KH * KW * C, M)), (wE, wi))
+    po = hf.conv2d(pi, pw, d)
+    out = hf.unpack(po, N * OH * OW, M, (wE, wo), kind="code")
+    torch.cuda.synchronize()
+    return codes_of(out).reshape(N, OH, OW, M)
+
+
+def test_small_conv_workload():
+    """8x8x4 IFM, eight 3x3x4 kernels, (5,3) inputs, (5,4) accumulation."""
+    hf = need_gpu()
+    ifm, w = I.small_conv_inputs()
+    qi, qw = orc.quantize_f32(ifm, 5, 3), orc.quantize_f32(w, 5, 3)
+    say("conv small workload")
+    got = run_conv(hf, qi, qw, 1, 1, 5, 3, 4, 4, 0)
+    want = orc.conv2d(qi, qw, 1, 1, 5, 3, 4, 4)
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("v", variants.CONV_VARIANTS, ids=variants.conv_tag)
+def test_conv_variants_vs_oracle(v):
+    """Every generated variant on a problem spanning two channel words and two
+    kernel words, both ragged, with padding and specials."""
+    hf = need_gpu()
+    wE, wi, wa, wo, act = v
+    g = np.random.default_rng([11, wi, wa, wo, act])
+    N, H, W, C, M = 2, 7, 9, 37, 40
+    ifm = I.inject_specials(g.uniform(-2, 2, (N, H, W, C)).astype(np.float32), g, 0.01)
+    w = I.inject_specials(g.uniform(-1, 1, (3, 3, C, M)).astype(np.float32), g, 0.005)
+    qi, qw = orc.quantize_f32(ifm, wE, wi), orc.quantize_f32(w, wE, wi)
+    for stride, pad in ((1, 1), (2, 0)):
+        say(f"conv variant {v} stride={stride} pad={pad}")
+        got = run_conv(hf, qi, qw, stride, pad, wE, wi, wa, wo, act)
+        want = orc.conv2d(qi, qw, stride, pad, wE, wi, wa, wo, act)
+        bad = np.argwhere(got != want)
+        assert bad.size == 0, f"{len(bad)} mismatches, first at {bad[0]}"
+
+
+def test_conv_1x1_and_raw_codes():
+    hf = need_gpu()
+    g = np.random.default_rng(5)
+    qi = I.random_codes(1, (3, 5, 4, 70), 11).astype(np.uint64)
+    qw = I.random_codes(2, (1, 1, 70, 33), 11).astype(np.uint64)
+    say("conv 1x1 raw codes")
+    got = run_conv(hf, qi, qw, 1, 0, 5, 3, 4, 4, 0)
+    want = orc.conv2d(qi, qw, 1, 0, 5, 3, 4, 4)
+    assert np.array_equal(got, want)
+
+
+def test_resnet_conv_layer_sampled():
+    """8x56x56x64 -> 64 kernels 3x3 in (5,3)/(5,4): every output computed on
+    the GPU, a sample (all four borders of every image plus random interior
+    points, every kernel) recomputed by the oracle."""
+    hf = need_gpu()
+    s = I.RESNET_CONV_SHAPE
+    ifm, w = I.resnet_conv_inputs()
+    qi, qw = orc.quantize_f32(ifm, 5, 3), orc.quantize_f32(w, 5, 3)
+    say("conv resnet layer 8x56x56x64->64")
+    got = run_conv(hf, qi, qw, 1, 1, 5, 3, 4, 4, 0)
+    g = np.random.default_rng(0)
+    pts = []
+    for n in range(s.N):
+        for t in range(s.OW):
+            for oy, ox in ((0, t), (s.OH - 1, t), (t, 0), (t, s.OW - 1)):
+                pts.append((n, oy, ox, g.integers(0, s.M)))
+    for _ in range(4096):
+        pts.append((g.integers(0, s.N), g.integers(0, s.OH), g.integers(0, s.OW), g.integers(0, s.M)))
+    pts = np.array(pts, np.int64)
+    want = orc.conv2d_points(qi, qw, pts, 1, 1, 5, 3, 4, 4)
+    gotp = got[pts[:, 0], pts[:, 1], pts[:, 2], pts[:, 3]]
+    assert np.array_equal(gotp, want)
