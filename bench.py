@@ -30,14 +30,24 @@ if ROOT not in sys.path:
 from paper_2007_06563_amd import hobflops as hf  # noqa: E402
 from paper_2007_06563_amd import inputs as I     # noqa: E402
 
-# MI355X: 256 CUs, 4 SIMDs of 16 lanes each (64 lanes/clk/CU for 32-bit VALU
-# ops), 2.4 GHz peak engine clock.
-N_CU, LANES_PER_CU_CLK, CLOCK_HZ = 256, 64, 2.4e9
-PEAK_LANE_OPS = N_CU * LANES_PER_CU_CLK * CLOCK_HZ   # 3.93e13 32-bit VALU ops/s
+# MI355X: 256 CUs of 4 SIMDs at up to 2.4 GHz. A SIMD retires 32 lanes of a
+# 32-bit VALU op per clock (128 lanes/clk/CU: the unit rate behind the
+# 157.3 TFLOP/s FP32-vector figure, one FMA = 2 flops), but one wave issues at
+# most one instruction every 4 clocks, i.e. half a SIMD: two or more waves per
+# SIMD are needed to reach the peak.
+N_CU, LANES_PER_CU_CLK, CLOCK_HZ = 256, 128, 2.4e9
+PEAK_LANE_OPS = N_CU * LANES_PER_CU_CLK * CLOCK_HZ   # 7.86e13 32-bit VALU ops/s
 N_SIMD = N_CU * 4
+SINGLE_WAVE_SHARE = 0.5
 HBM_PEAK = 8.0e12
 
 IN_FMT, ACC_FMT, OUT_FMT = (5, 3), (5, 4), (5, 4)
+
+# HBM bytes per launch of the convolution kernel from rocprofv3 --pmc
+# FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by what the same
+# counter reads for a plain 256 MiB device copy (FETCH x2.0, WRITE x1.0); see
+# the profiles/ summaries. None once the kernel has changed since.
+TRAFFIC = None
 
 
 def log(*a):
@@ -102,6 +112,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB "
+                         "(steps times): the reference for scaling HBM byte counters")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the layer shards "
@@ -110,6 +123,15 @@ def main():
         sys.exit(2)
     torch.cuda.init()
     dev = torch.device("cuda:0")
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(args.steps):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibration_copy_bytes_each_way": n * 4, "launches": args.steps}))
+        return
     s = I.RESNET_CONV_SHAPE
     ifm, w = I.resnet_conv_inputs()
     d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, IN_FMT, ACC_FMT,
@@ -183,9 +205,10 @@ def main():
                    "macs_per_step": macs, "batch": s.N},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
                      "unit": "T VALU-op/s (32-bit bitwise, one op = 32 gates)",
-                     "frac": achieved / PEAK_LANE_OPS, "traffic": None,
+                     "frac": achieved / PEAK_LANE_OPS, "traffic": TRAFFIC,
                      "kernel": "conv2d_kernel", "ops_per_mac_word": G,
-                     "kernel_ms": conv_ms, "wave_ceiling": min(1.0, waves / N_SIMD)},
+                     "kernel_ms": conv_ms,
+                     "issue_ceiling": min(1.0, waves * SINGLE_WAVE_SHARE / N_SIMD)},
         "pct_valu_peak": 100.0 * achieved / PEAK_LANE_OPS,
         "conv_gmacs": macs / (conv_ms * 1e-3) / 1e9,
         "pack_ms": pack_ms, "unpack_ms": unpack_ms,

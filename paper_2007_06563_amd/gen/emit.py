@@ -60,10 +60,26 @@ def schedule(C):
     return order
 
 
+def output_polarity(C):
+    """Nodes to emit complemented: those whose every use as an output is
+    complemented (a LUT computes either polarity at the same cost, and LUT
+    consumers absorb the flip into their truth tables)."""
+    pos, neg = set(), set()
+    for _, lits in C.outputs:
+        for l in lits:
+            n = l >> 1
+            if n == 0 or C.is_input[n]:
+                continue
+            (neg if (l & 1) else pos).add(n)
+    return neg - pos
+
+
 def emit_function(C, fname, in_place=None):
     """C++ text of one __device__ function. Inputs are const array references
     in port order; the output group is a reference array. If in_place names an
     input group, the output overwrites that input array."""
+    from .circuit import tt_flip
+    flipped = output_polarity(C)
     names = {}
     params = []
     loads = []
@@ -84,16 +100,22 @@ def emit_function(C, fname, in_place=None):
     body = []
     for n in schedule(C):
         fan = C.fanins[n]
+        k = len(fan)
         tt = C.tts[n]
+        for i, f in enumerate(fan):  # fan-ins emitted complemented
+            if f in flipped:
+                tt = tt_flip(tt, k, i)
+        if n in flipped:
+            tt = ~tt & ((1 << (1 << k)) - 1)
         v = f"t{n}"
         names[n] = v
         args = [names[f] for f in fan]
-        if len(fan) == 3:
+        if k == 3:
             expr = f"__builtin_amdgcn_bitop3_b32({args[2]}, {args[1]}, {args[0]}, 0x{tt:02x})"
-        elif len(fan) == 2:
+        elif k == 2:
             expr = TWO_INPUT[tt].format(a=args[0], b=args[1])
         else:
-            raise ValueError(f"unexpected node arity {len(fan)}")
+            raise ValueError(f"unexpected node arity {k}")
         body.append(f"  const uint32_t {v} = {expr};")
     stores = []
     for group, lits in outs:
@@ -102,18 +124,22 @@ def emit_function(C, fname, in_place=None):
             if n == 0:
                 val = "0xffffffffu" if (l & 1) else "0u"
             else:
-                val = ("~" if (l & 1) else "") + names[n]
+                inv = (l & 1) ^ (1 if n in flipped else 0)
+                val = ("~" if inv else "") + names[n]
             stores.append(f"  {group}[{b}] = {val};")
     head = f"static __device__ __forceinline__ void {fname}({', '.join(params)})\n{{"
     return "\n".join([head] + loads + body + stores + ["}"]) + "\n"
 
 
 def op_count(C):
-    """VALU instructions the emitted function executes: one per node plus one
-    NOT per complemented output of a non-constant node."""
+    """VALU instructions the emitted function executes: one per node, plus one
+    NOT per output that needs the other polarity of what its node is emitted
+    in (an input copied out complemented, or a node used in both polarities)."""
+    flipped = output_polarity(C)
     n = C.n_nodes()
     for _, lits in C.outputs:
         for l in lits:
-            if (l & 1) and (l >> 1) != 0:
+            node = l >> 1
+            if node != 0 and (l & 1) ^ (1 if node in flipped else 0):
                 n += 1
     return n
