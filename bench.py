@@ -134,9 +134,14 @@ def main():
         return
     s = I.RESNET_CONV_SHAPE
     ifm, w = I.resnet_conv_inputs()
-    d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, IN_FMT, ACC_FMT,
-                     OUT_FMT, hf.ACT_NONE)
     P = s.N * s.OH * s.OW
+    # the library's automatic choice: split multiply/accumulate waves when the
+    # accumulator waves would leave each SIMD at most one
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+    chain_waves = ((P + 63) // 64) * ((s.M + 31) // 32)
+    algo = hf.ALGO_SPLIT if chain_waves <= 4 * cus else hf.ALGO_FUSED
+    d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, IN_FMT, ACC_FMT,
+                     OUT_FMT, hf.ACT_NONE, algo)
     x_ifm = torch.from_numpy(ifm.reshape(s.N * s.H * s.W, s.C)).to(dev)
     x_w = torch.from_numpy(w.reshape(s.KH * s.KW * s.C, s.M)).to(dev)
     p_ifm = torch.empty(hf.plane_shape(s.N * s.H * s.W, s.C, IN_FMT), dtype=torch.int32, device=dev)
@@ -175,7 +180,8 @@ def main():
     unpack_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
 
     macs = s.macs
-    G, _ = hf.netlist_ops(IN_FMT, ACC_FMT)
+    ops = hf.netlist_ops(IN_FMT, ACC_FMT)
+    G = ops["mul"] + ops["accum"] if algo == hf.ALGO_SPLIT else ops["mac"]
     lane_ops = macs / 32.0 * G          # 32 MACs per 32-bit word operation
     achieved = lane_ops / (conv_ms * 1e-3)
     waves = ((P + 63) // 64) * ((s.M + 31) // 32)
@@ -206,9 +212,11 @@ def main():
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
                      "unit": "T VALU-op/s (32-bit bitwise, one op = 32 gates)",
                      "frac": achieved / PEAK_LANE_OPS, "traffic": TRAFFIC,
-                     "kernel": "conv2d_kernel", "ops_per_mac_word": G,
+                     "kernel": "conv2d_split_kernel" if algo == hf.ALGO_SPLIT else "conv2d_kernel",
+                     "ops_per_mac_word": G,
                      "kernel_ms": conv_ms,
-                     "issue_ceiling": min(1.0, waves * SINGLE_WAVE_SHARE / N_SIMD)},
+                     "issue_ceiling": min(1.0, waves * SINGLE_WAVE_SHARE / N_SIMD) if algo ==
+                     hf.ALGO_FUSED else None},
         "pct_valu_peak": 100.0 * achieved / PEAK_LANE_OPS,
         "conv_gmacs": macs / (conv_ms * 1e-3) / 1e9,
         "pack_ms": pack_ms, "unpack_ms": unpack_ms,

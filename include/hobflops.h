@@ -59,6 +59,12 @@ enum { HOBFLOPS_SRC_F32 = 0, HOBFLOPS_SRC_CODE_U32 = 1 };
 enum { HOBFLOPS_ROUND_NEAREST_EVEN = 0 };
 enum { HOBFLOPS_ORDER_KY_KX_C = 0 };
 enum { HOBFLOPS_ACT_NONE = 0, HOBFLOPS_ACT_RELU = 1 };
+/* Kernel shape of hobflops_conv2d (results are identical for all three):
+ * AUTO picks SPLIT when the launch has at most one accumulator wave per SIMD
+ * of the device and FUSED otherwise; FUSED runs multiplier and adder on the
+ * same wave; SPLIT runs them on separate waves of the same CU so that a
+ * launch with few accumulator chains can still fill the VALU. */
+enum { HOBFLOPS_ALGO_AUTO = 0, HOBFLOPS_ALGO_FUSED = 1, HOBFLOPS_ALGO_SPLIT = 2 };
 
 /* Number of uint32 words of a PL32 tensor: rows * ceil(len/32) * NB.
  * Returns HOBFLOPS_OK and writes *words, or HOBFLOPS_EINVAL. */
@@ -97,6 +103,7 @@ typedef struct {
   int N, H, W, C, M, KH, KW, stride, pad;
   hobflops_fmt in_fmt, acc_fmt, out_fmt;
   int act, round, order;
+  int algo; /* HOBFLOPS_ALGO_* */
 } hobflops_conv_desc;
 
 int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
@@ -117,11 +124,12 @@ int hobflops_muladd_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt);
 
 /* Bitwise VALU instructions per 32-lane word in the generated netlists of a
  * MAC (in_fmt x in_fmt -> acc_fmt, then acc_fmt + acc_fmt): the convolution's
- * fused step, and the element-wise kernel's (the paper's gate count,
- * Sec. 4: throughput follows it). Returns HOBFLOPS_OK or
+ * fused multiply-add step, its multiplier and its accumulating adder alone
+ * (the split kernel's two wave roles), and the element-wise kernel's MAC (the
+ * paper's gate count, Sec. 4: throughput follows it). Returns HOBFLOPS_OK or
  * HOBFLOPS_EUNSUPPORTED; any output pointer may be NULL. */
 int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int* conv_mac_ops,
-                         int* muladd_ops);
+                         int* conv_mul_ops, int* conv_accum_ops, int* muladd_ops);
 
 /* Text for a status code; for HOBFLOPS_EHIP, the last HIP error of this
  * thread. The pointer stays valid until the next call on the same thread. */

@@ -28,7 +28,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 from paper_2007_06563_amd import variants  # noqa: E402
-from paper_2007_06563_amd.gen import emit, fp, opt  # noqa: E402
+from paper_2007_06563_amd.gen import asmgen, emit, fp, opt  # noqa: E402
 
 
 def nb(wE, wF):
@@ -37,14 +37,15 @@ def nb(wE, wF):
 
 def _gen_sources_digest():
     h = hashlib.sha256()
-    for name in ("circuit.py", "fp.py", "opt.py", "emit.py"):
+    for name in ("circuit.py", "fp.py", "opt.py", "emit.py", "regalloc.py", "asmgen.py"):
         h.update(open(os.path.join(HERE, "gen", name), "rb").read())
     return h.hexdigest()[:16]
 
 
 def netlist(kind, key, cache):
     """Optimised circuit for one operator; cached per generator version."""
-    name = {"mac": "mac_e{}m{}_a{}", "epi": "epi_e{}m{}_o{}{}", "muladd": "muladd_e{}m{}_a{}"}[kind]
+    name = {"mac": "mac_e{}m{}_a{}", "epi": "epi_e{}m{}_o{}{}", "muladd": "muladd_e{}m{}_a{}",
+            "prod": "prod_e{}m{}_a{}", "accum": "accum_e{}m{}"}[kind]
     if kind == "epi":
         wE, wa, wo, act = key
         fname = name.format(wE, wa, wo, "_relu" if act else "")
@@ -54,6 +55,12 @@ def netlist(kind, key, cache):
         return fname, cache[fname]
     if kind == "mac":
         C = fp.mac_circuit(*key)
+        text_kw = {"in_place": "acc"}
+    elif kind == "prod":
+        C = fp.product_circuit(*key)
+        text_kw = {}
+    elif kind == "accum":
+        C = fp.accumulate_circuit(*key)
         text_kw = {"in_place": "acc"}
     elif kind == "epi":
         wE, wa, wo, act = key
@@ -68,6 +75,24 @@ def netlist(kind, key, cache):
              "raw_nodes": raw}
     cache[fname] = entry
     return fname, entry
+
+
+def split_batch(naccp):
+    """Products per barrier in the split kernel (even; the LDS ring of
+    2 x batch x 256 lanes x entry words must stay within 128 KiB)."""
+    return 4 if naccp <= 16 else 2
+
+
+def split_asm(wE, wi, wa, cache):
+    key = f"split_e{wE}m{wi}_a{wa}"
+    if key not in cache:
+        nin, nacc = nb(wE, wi), nb(wE, wa)
+        acc_c = opt.optimize(fp.accumulate_circuit(wE, wa))
+        prod_c = opt.optimize(fp.product_circuit(wE, wi, wa))
+        text, stats = asmgen.split_functions(acc_c, prod_c, nin, nacc,
+                                             split_batch(asmgen.pad4(nacc)))
+        cache[key] = {"text": text, "stats": stats}
+    return cache[key]
 
 
 def generate(verbose=True):
@@ -86,6 +111,9 @@ def generate(verbose=True):
         tag = variants.conv_tag(v)
         mac, mac_e = netlist("mac", (wE, wi, wa), cache)
         epi, _ = netlist("epi", (wE, wa, wo, act), cache)
+        prod, prod_e = netlist("prod", (wE, wi, wa), cache)
+        accum, accum_e = netlist("accum", (wE, wa), cache)
+        sp = split_asm(wE, wi, wa, cache)
         src = f"""// Generated: convolution variant {tag}. Do not edit.
 #include "kernels.hpp"
 #include "registry.hpp"
@@ -93,25 +121,53 @@ namespace hobflops {{
 namespace conv_{tag} {{
 {cache[mac]['text']}
 {cache[epi]['text']}
+{cache[prod]['text']}
+{cache[accum]['text']}
+{sp['text']}
 struct V {{
   static constexpr int NIN = {nb(wE, wi)}, NACC = {nb(wE, wa)}, NOUT = {nb(wE, wo)};
+  static constexpr int kBatch = {split_batch(asmgen.pad4(nb(wE, wa)))};
+  static constexpr const int* kAccSlot = conv_{tag}::kAccSlot;
+  static constexpr const int* kProdSlot = conv_{tag}::kProdSlot;
+  static constexpr const int* kWSlot = conv_{tag}::kWSlot;
+  static __device__ __forceinline__ void accum_batch(uint32_t (&acc)[(NACC + 3) & ~3],
+                                                     const lds_u32* entry) {{
+    conv_{tag}::accum_batch(acc, entry);
+  }}
+  static __device__ __forceinline__ void product_step(const uint32_t (&xw)[NIN], int c,
+                                                      const lds_u32* wrow, lds_u32* entry) {{
+    conv_{tag}::product_step(xw, c, wrow, entry);
+  }}
+  static __device__ __forceinline__ void product_batch(const uint32_t (&xw)[NIN], int c,
+                                                       const lds_u32* wrow, lds_u32* entry) {{
+    conv_{tag}::product_batch(xw, c, wrow, entry);
+  }}
   static __device__ __forceinline__ void mac(uint32_t (&acc)[NACC], const uint32_t (&w)[NIN],
                                              const uint32_t (&x)[NIN]) {{ {mac}(acc, w, x); }}
+  static __device__ __forceinline__ void mul(const uint32_t (&w)[NIN], const uint32_t (&x)[NIN],
+                                             uint32_t (&p)[NACC]) {{ {prod}(w, x, p); }}
+  static __device__ __forceinline__ void add(uint32_t (&acc)[NACC], const uint32_t (&p)[NACC]) {{
+    {accum}(acc, p);
+  }}
   static __device__ __forceinline__ void epi(const uint32_t (&acc)[NACC], uint32_t (&out)[NOUT]) {{
     {epi}(acc, out);
   }}
 }};
 }}  // namespace conv_{tag}
 hipError_t launch_conv_{tag}(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
-                              const ConvParams& p, hipStream_t stream) {{
+                              const ConvParams& p, int algo, hipStream_t stream) {{
   dim3 grid((unsigned)((p.P + kConvBlock - 1) / kConvBlock), (unsigned)p.MT);
-  hipLaunchKernelGGL(conv2d_kernel<conv_{tag}::V>, grid, dim3(kConvBlock), 0, stream, ifm, w, ofm, p);
+  if (algo == kAlgoSplit)
+    hipLaunchKernelGGL(conv2d_split_kernel<conv_{tag}::V>, grid, dim3(2 * kConvBlock), 0, stream,
+                       ifm, w, ofm, p);
+  else
+    hipLaunchKernelGGL(conv2d_kernel<conv_{tag}::V>, grid, dim3(kConvBlock), 0, stream, ifm, w, ofm, p);
   return hipGetLastError();
 }}
 }}  // namespace hobflops
 """
         files.append((f"conv_{tag}.hip", src))
-        reg_conv.append((v, tag, mac_e["ops"]))
+        reg_conv.append((v, tag, mac_e["ops"], prod_e["ops"], accum_e["ops"]))
     for v in variants.MULADD_VARIANTS:
         wE, wi, wa = v
         tag = variants.muladd_tag(v)
@@ -142,15 +198,16 @@ hipError_t launch_muladd_{tag}(const uint32_t* a, const uint32_t* b, const uint3
         reg_mul.append((v, tag, e["ops"]))
     reg = ["// Generated: table of kernel variants (host code). Do not edit.",
            '#include "registry.hpp"', "#ifndef __HIP_DEVICE_COMPILE__", "namespace hobflops {"]
-    for v, tag, ops in reg_conv:
+    for v, tag, *_ in reg_conv:
         reg.append(f"hipError_t launch_conv_{tag}(const uint32_t*, const uint32_t*, uint32_t*, "
-                   f"const ConvParams&, hipStream_t);")
+                   f"const ConvParams&, int, hipStream_t);")
     for v, tag, ops in reg_mul:
         reg.append(f"hipError_t launch_muladd_{tag}(const uint32_t*, const uint32_t*, const uint32_t*, "
                    f"uint32_t*, int64_t, hipStream_t);")
     reg.append("const ConvVariant kConvVariants[] = {")
-    for v, tag, ops in reg_conv:
-        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {v[4]}, {ops}, launch_conv_{tag}}},")
+    for v, tag, ops, pops, aops in reg_conv:
+        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {v[4]}, {ops}, {pops}, {aops}, "
+                   f"launch_conv_{tag}}},")
     reg.append("};")
     reg.append(f"const int kNumConvVariants = {len(reg_conv)};")
     reg.append("const MuladdVariant kMuladdVariants[] = {")
@@ -167,11 +224,16 @@ hipError_t launch_muladd_{tag}(const uint32_t* a, const uint32_t* b, const uint3
             with open(path, "w") as f:
                 f.write(text)
     json.dump({"digest": digest, "netlists": cache}, open(cache_path, "w"))
-    gates = {k: {"ops": e["ops"], "raw_nodes": e["raw_nodes"]} for k, e in cache.items()}
+    gates = {k: ({"ops": e["ops"], "raw_nodes": e["raw_nodes"]} if "ops" in e else e["stats"])
+             for k, e in cache.items()}
     json.dump(gates, open(os.path.join(GEN, "gates.json"), "w"), indent=1, sort_keys=True)
     if verbose:
         for k in sorted(gates):
-            print(f"  {k}: {gates[k]['ops']} ops (raw {gates[k]['raw_nodes']})")
+            g = gates[k]
+            if "ops" in g:
+                print(f"  {k}: {g['ops']} ops (raw {g['raw_nodes']})")
+            else:
+                print(f"  {k}: accum {g['accum']}, mul {g['mul']}")
     return [os.path.join(GEN, n) for n, _ in files]
 
 

@@ -58,6 +58,9 @@ int conv_check(const hobflops_conv_desc* d) {
   if (d->act != HOBFLOPS_ACT_NONE && d->act != HOBFLOPS_ACT_RELU) return HOBFLOPS_EINVAL;
   if (d->round != HOBFLOPS_ROUND_NEAREST_EVEN || d->order != HOBFLOPS_ORDER_KY_KX_C)
     return HOBFLOPS_EINVAL;
+  if (d->algo != HOBFLOPS_ALGO_AUTO && d->algo != HOBFLOPS_ALGO_FUSED &&
+      d->algo != HOBFLOPS_ALGO_SPLIT)
+    return HOBFLOPS_EINVAL;
   const int64_t OH = (d->H + 2 * (int64_t)d->pad - d->KH) / d->stride + 1;
   const int64_t OW = (d->W + 2 * (int64_t)d->pad - d->KW) / d->stride + 1;
   const int64_t P = (int64_t)d->N * OH * OW;
@@ -131,7 +134,19 @@ int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
   p.CG = (d->C + 31) / 32;
   p.MT = (d->M + 31) / 32;
   p.P = p.N * p.OH * p.OW;
-  return hip_status(v->launch(ifm, w, ofm, p, (hipStream_t)stream));
+  int algo = d->algo;
+  if (algo == HOBFLOPS_ALGO_AUTO) {
+    // one accumulator wave per 64 positions and m-tile; split when they would
+    // leave the SIMDs of the device at most one each
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_status(e);
+    const int64_t chain_waves = (int64_t)((p.P + 63) / 64) * p.MT;
+    algo = chain_waves <= 4 * (int64_t)cus ? HOBFLOPS_ALGO_SPLIT : HOBFLOPS_ALGO_FUSED;
+  }
+  return hip_status(v->launch(ifm, w, ofm, p, algo == HOBFLOPS_ALGO_SPLIT ? kAlgoSplit : kAlgoFused,
+                              (hipStream_t)stream));
 }
 
 int hobflops_muladd_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt) {
@@ -151,15 +166,19 @@ int hobflops_muladd(const uint32_t* a, const uint32_t* b, const uint32_t* c, uin
 }
 
 int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int* conv_mac_ops,
-                         int* muladd_ops) {
+                         int* conv_mul_ops, int* conv_accum_ops, int* muladd_ops) {
   int found = 0;
   if (conv_mac_ops) *conv_mac_ops = 0;
+  if (conv_mul_ops) *conv_mul_ops = 0;
+  if (conv_accum_ops) *conv_accum_ops = 0;
   if (muladd_ops) *muladd_ops = 0;
   for (int i = 0; i < kNumConvVariants; ++i) {
     const ConvVariant& v = kConvVariants[i];
     if (v.wE == in_fmt.wE && v.wF_in == in_fmt.wF && v.wF_acc == acc_fmt.wF &&
         acc_fmt.wE == in_fmt.wE) {
       if (conv_mac_ops) *conv_mac_ops = v.mac_ops;
+      if (conv_mul_ops) *conv_mul_ops = v.mul_ops;
+      if (conv_accum_ops) *conv_accum_ops = v.accum_ops;
       found = 1;
       break;
     }

@@ -17,6 +17,7 @@ _lib = None
 SRC_F32, SRC_CODE_U32 = 0, 1
 ACT_NONE, ACT_RELU = 0, 1
 ROUND_NEAREST_EVEN, ORDER_KY_KX_C = 0, 0
+ALGO_AUTO, ALGO_FUSED, ALGO_SPLIT = 0, 1, 2
 
 
 class HobflopsError(RuntimeError):
@@ -37,7 +38,8 @@ class ConvDesc(ctypes.Structure):
                 ("C", ctypes.c_int), ("M", ctypes.c_int), ("KH", ctypes.c_int),
                 ("KW", ctypes.c_int), ("stride", ctypes.c_int), ("pad", ctypes.c_int),
                 ("in_fmt", Fmt), ("acc_fmt", Fmt), ("out_fmt", Fmt),
-                ("act", ctypes.c_int), ("round", ctypes.c_int), ("order", ctypes.c_int)]
+                ("act", ctypes.c_int), ("round", ctypes.c_int), ("order", ctypes.c_int),
+                ("algo", ctypes.c_int)]
 
 
 EXPORTS = ("hobflops_plane_words", "hobflops_pack", "hobflops_unpack", "hobflops_conv2d",
@@ -61,7 +63,7 @@ def lib():
         L.hobflops_conv2d_supported.argtypes = [ctypes.POINTER(ConvDesc)]
         L.hobflops_muladd.argtypes = [vp, vp, vp, vp, i64, Fmt, Fmt, vp]
         L.hobflops_muladd_supported.argtypes = [Fmt, Fmt]
-        L.hobflops_netlist_ops.argtypes = [Fmt, Fmt, ctypes.POINTER(ci), ctypes.POINTER(ci)]
+        L.hobflops_netlist_ops.argtypes = [Fmt, Fmt] + [ctypes.POINTER(ci)] * 4
         L.hobflops_status_string.argtypes = [ci]
         L.hobflops_status_string.restype = ctypes.c_char_p
         for name in EXPORTS[:-1]:
@@ -139,9 +141,10 @@ def unpack(planes, rows, length, f, kind="f32", out=None):
     return out
 
 
-def conv_desc(N, H, W, C, M, KH, KW, stride, pad, in_fmt, acc_fmt, out_fmt, act=ACT_NONE):
+def conv_desc(N, H, W, C, M, KH, KW, stride, pad, in_fmt, acc_fmt, out_fmt, act=ACT_NONE,
+              algo=ALGO_AUTO):
     return ConvDesc(N, H, W, C, M, KH, KW, stride, pad, fmt(in_fmt), fmt(acc_fmt), fmt(out_fmt),
-                    act, ROUND_NEAREST_EVEN, ORDER_KY_KX_C)
+                    act, ROUND_NEAREST_EVEN, ORDER_KY_KX_C, algo)
 
 
 def conv_out_hw(d):
@@ -178,9 +181,10 @@ def muladd_supported(in_fmt, acc_fmt):
 
 
 def netlist_ops(in_fmt, acc_fmt):
-    """(conv MAC ops, element-wise MAC ops) per 32-lane word; 0 where not generated."""
-    a, b = ctypes.c_int(), ctypes.c_int()
-    rc = lib().hobflops_netlist_ops(fmt(in_fmt), fmt(acc_fmt), ctypes.byref(a), ctypes.byref(b))
+    """dict of VALU ops per 32-lane word: conv 'mac' (fused step), 'mul' and 'accum'
+    (the split kernel's two roles), element-wise 'muladd'; 0 where not generated."""
+    v = [ctypes.c_int() for _ in range(4)]
+    rc = lib().hobflops_netlist_ops(fmt(in_fmt), fmt(acc_fmt), *[ctypes.byref(x) for x in v])
     if rc != 0:
         raise HobflopsError(rc, lib().hobflops_status_string(rc).decode())
-    return a.value, b.value
+    return dict(zip(("mac", "mul", "accum", "muladd"), (x.value for x in v)))

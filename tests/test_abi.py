@@ -64,13 +64,11 @@ def test_conv_rejects_bad_descriptors(hf, bad):
     assert not hf.conv2d_supported(d)
 
 
-def test_conv_rejects_round_and_order(hf):
-    d = desc(hf)
-    d.round = 1
-    assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -1
-    d = desc(hf)
-    d.order = 2
-    assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -1
+def test_conv_rejects_round_order_and_algo(hf):
+    for field, value in (("round", 1), ("order", 2), ("algo", 3), ("algo", -1)):
+        d = desc(hf)
+        setattr(d, field, value)
+        assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -1, field
 
 
 def test_conv_null_misaligned_unsupported(hf):
@@ -110,8 +108,9 @@ def test_muladd_argument_checks(hf):
 
 
 def test_netlist_ops_and_status_strings(hf):
-    conv_ops, mul_ops = hf.netlist_ops((5, 3), (5, 4))
-    assert 50 < conv_ops < 1000 and 50 < mul_ops < 1000
+    ops = hf.netlist_ops((5, 3), (5, 4))
+    assert 50 < ops["mac"] < 1000 and 50 < ops["muladd"] < 1000
+    assert 20 < ops["mul"] < ops["mac"] and 50 < ops["accum"] < ops["mac"]
     with pytest.raises(hf.HobflopsError):
         hf.netlist_ops((5, 3), (5, 9))
     L = hf.lib()

@@ -109,11 +109,11 @@ def test_muladd_raw_codes_vs_oracle(v):
     assert np.array_equal(got, want)
 
 
-def run_conv(hf, ifm_codes, w_codes, stride, pad, wE, wi, wa, wo, act):
+def run_conv(hf, ifm_codes, w_codes, stride, pad, wE, wi, wa, wo, act, algo=0):
     """GPU conv on code tensors (NHWC / HWIO) -> output codes [N, OH, OW, M]."""
     N, H, W, C = ifm_codes.shape
     KH, KW, _, M = w_codes.shape
-    d = hf.conv_desc(N, H, W, C, M, KH, KW, stride, pad, (wE, wi), (wE, wa), (wE, wo), act)
+    d = hf.conv_desc(N, H, W, C, M, KH, KW, stride, pad, (wE, wi), (wE, wa), (wE, wo), act, algo)
     OH, OW = hf.conv_out_hw(d)
     pi = hf.pack(dev(ifm_codes.astype(np.uint32).view(np.int32).reshape(N * H * W, C)), (wE, wi))
     pw = hf.pack(dev(w_codes.astype(np.uint32).view(np.int32).reshape(KH * KW * C, M)), (wE, wi))
@@ -134,10 +134,11 @@ def test_small_conv_workload():
     assert np.array_equal(got, want)
 
 
+@pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
 @pytest.mark.parametrize("v", variants.CONV_VARIANTS, ids=variants.conv_tag)
-def test_conv_variants_vs_oracle(v):
-    """Every generated variant on a problem spanning two channel words and two
-    kernel words, both ragged, with padding and specials."""
+def test_conv_variants_vs_oracle(v, algo):
+    """Every generated variant, in both kernel shapes, on a problem spanning two
+    channel words and two kernel words, both ragged, with padding and specials."""
     hf = need_gpu()
     wE, wi, wa, wo, act = v
     g = np.random.default_rng([11, wi, wa, wo, act])
@@ -146,22 +147,36 @@ def test_conv_variants_vs_oracle(v):
     w = I.inject_specials(g.uniform(-1, 1, (3, 3, C, M)).astype(np.float32), g, 0.005)
     qi, qw = orc.quantize_f32(ifm, wE, wi), orc.quantize_f32(w, wE, wi)
     for stride, pad in ((1, 1), (2, 0)):
-        say(f"conv variant {v} stride={stride} pad={pad}")
-        got = run_conv(hf, qi, qw, stride, pad, wE, wi, wa, wo, act)
+        say(f"conv variant {v} algo={algo} stride={stride} pad={pad}")
+        got = run_conv(hf, qi, qw, stride, pad, wE, wi, wa, wo, act, algo)
         want = orc.conv2d(qi, qw, stride, pad, wE, wi, wa, wo, act)
         bad = np.argwhere(got != want)
         assert bad.size == 0, f"{len(bad)} mismatches, first at {bad[0]}"
 
 
-def test_conv_1x1_and_raw_codes():
+@pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
+def test_conv_1x1_and_raw_codes(algo):
     hf = need_gpu()
-    g = np.random.default_rng(5)
     qi = I.random_codes(1, (3, 5, 4, 70), 11).astype(np.uint64)
     qw = I.random_codes(2, (1, 1, 70, 33), 11).astype(np.uint64)
-    say("conv 1x1 raw codes")
-    got = run_conv(hf, qi, qw, 1, 0, 5, 3, 4, 4, 0)
+    say(f"conv 1x1 raw codes algo={algo}")
+    got = run_conv(hf, qi, qw, 1, 0, 5, 3, 4, 4, 0, algo)
     want = orc.conv2d(qi, qw, 1, 0, 5, 3, 4, 4)
     assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
+def test_conv_tap_counts_not_multiple_of_batch(algo):
+    """C = 3 with a 3x3 kernel (27 taps) and C = 5 with 1x1 (5 taps): batches and
+    channel words end at different taps."""
+    hf = need_gpu()
+    g = np.random.default_rng(9)
+    for (N, H, W, C, M, k, pad) in ((2, 9, 11, 3, 36, 3, 1), (1, 4, 4, 5, 7, 1, 0)):
+        qi = orc.quantize_f32(g.uniform(-2, 2, (N, H, W, C)).astype(np.float32), 5, 3)
+        qw = orc.quantize_f32(g.uniform(-1, 1, (k, k, C, M)).astype(np.float32), 5, 3)
+        say(f"conv taps C={C} k={k} algo={algo}")
+        got = run_conv(hf, qi, qw, 1, pad, 5, 3, 4, 4, 0, algo)
+        assert np.array_equal(got, orc.conv2d(qi, qw, 1, pad, 5, 3, 4, 4))
 
 
 def test_resnet_conv_layer_sampled():
