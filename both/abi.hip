@@ -1,0 +1,205 @@
+// C ABI of libhobflops.so (declared in include/hobflops.h): argument checks,
+// variant dispatch and launches. Nothing here computes on the host.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "hobflops.h"
+#include "pack.hpp"
+#include "registry.hpp"
+
+using namespace hobflops;
+
+namespace {
+
+thread_local char g_errbuf[256];
+
+int fmt_ok(hobflops_fmt f) {
+  return f.wE >= 2 && f.wE <= 8 && f.wF >= 1 && f.wF <= 23 && 3 + f.wE + f.wF <= 32;
+}
+int aligned(const void* p) { return ((uintptr_t)p & 3u) == 0; }
+
+int hip_status(hipError_t e) {
+  if (e == hipSuccess) return HOBFLOPS_OK;
+  snprintf(g_errbuf, sizeof g_errbuf, "HIP error %d: %s", (int)e, hipGetErrorString(e));
+  return HOBFLOPS_EHIP;
+}
+
+const ConvVariant* find_conv(const hobflops_conv_desc* d) {
+  for (int i = 0; i < kNumConvVariants; ++i) {
+    const ConvVariant& v = kConvVariants[i];
+    if (v.wE == d->in_fmt.wE && v.wF_in == d->in_fmt.wF && v.wF_acc == d->acc_fmt.wF &&
+        v.wF_out == d->out_fmt.wF && v.act == d->act)
+      return &v;
+  }
+  return nullptr;
+}
+
+const MuladdVariant* find_muladd(hobflops_fmt in, hobflops_fmt acc) {
+  for (int i = 0; i < kNumMuladdVariants; ++i) {
+    const MuladdVariant& v = kMuladdVariants[i];
+    if (v.wE == in.wE && v.wF_in == in.wF && v.wF_acc == acc.wF && acc.wE == in.wE) return &v;
+  }
+  return nullptr;
+}
+
+// Shape and format checks shared by conv2d and conv2d_supported.
+int conv_check(const hobflops_conv_desc* d) {
+  if (!d) return HOBFLOPS_EINVAL;
+  if (d->N < 1 || d->H < 1 || d->W < 1 || d->C < 1 || d->M < 1 || d->KH < 1 || d->KW < 1 ||
+      d->stride < 1 || d->pad < 0)
+    return HOBFLOPS_EINVAL;
+  if (d->H + 2 * (int64_t)d->pad < d->KH || d->W + 2 * (int64_t)d->pad < d->KW)
+    return HOBFLOPS_EINVAL;
+  if (!fmt_ok(d->in_fmt) || !fmt_ok(d->acc_fmt) || !fmt_ok(d->out_fmt)) return HOBFLOPS_EINVAL;
+  if (d->acc_fmt.wE != d->in_fmt.wE || d->out_fmt.wE != d->in_fmt.wE) return HOBFLOPS_EINVAL;
+  if (d->acc_fmt.wF < d->in_fmt.wF) return HOBFLOPS_EINVAL;
+  if (d->act != HOBFLOPS_ACT_NONE && d->act != HOBFLOPS_ACT_RELU) return HOBFLOPS_EINVAL;
+  if (d->round != HOBFLOPS_ROUND_NEAREST_EVEN || d->order != HOBFLOPS_ORDER_KY_KX_C)
+    return HOBFLOPS_EINVAL;
+  if (d->algo != HOBFLOPS_ALGO_AUTO && d->algo != HOBFLOPS_ALGO_FUSED &&
+      d->algo != HOBFLOPS_ALGO_SPLIT)
+    return HOBFLOPS_EINVAL;
+  const int64_t OH = (d->H + 2 * (int64_t)d->pad - d->KH) / d->stride + 1;
+  const int64_t OW = (d->W + 2 * (int64_t)d->pad - d->KW) / d->stride + 1;
+  const int64_t P = (int64_t)d->N * OH * OW;
+  const int64_t MT = (d->M + 31) / 32;
+  // index arithmetic inside the kernel is 32-bit for positions and taps
+  if (P > (int64_t)1 << 30 || (int64_t)d->N * d->H * d->W > (int64_t)1 << 30 ||
+      (int64_t)d->KH * d->KW * d->C > (int64_t)1 << 24 || MT > 65535)
+    return HOBFLOPS_EINVAL;
+  return HOBFLOPS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int hobflops_plane_words(int64_t rows, int64_t len, hobflops_fmt f, int64_t* words) {
+  if (!words || rows < 0 || len < 0 || !fmt_ok(f)) return HOBFLOPS_EINVAL;
+  const int64_t G = (len + 31) / 32;
+  const int64_t nb = 3 + f.wE + f.wF;
+  if (rows > 0 && G > INT64_MAX / nb / rows) return HOBFLOPS_EINVAL;
+  *words = rows * G * nb;
+  return HOBFLOPS_OK;
+}
+
+int hobflops_pack(const void* src, int kind, int64_t rows, int64_t len, hobflops_fmt f,
+                  uint32_t* planes, void* stream) {
+  if (rows < 0 || len < 0 || !fmt_ok(f)) return HOBFLOPS_EINVAL;
+  if (kind != HOBFLOPS_SRC_F32 && kind != HOBFLOPS_SRC_CODE_U32) return HOBFLOPS_EINVAL;
+  if (rows == 0 || len == 0) return HOBFLOPS_OK;
+  if (!src || !planes) return HOBFLOPS_EINVAL;
+  if (!aligned(src) || !aligned(planes)) return HOBFLOPS_EALIGN;
+  if ((len + 31) / 32 > INT32_MAX) return HOBFLOPS_EINVAL;
+  return hip_status(launch_pack(src, kind, rows, len, f.wE, f.wF, planes, (hipStream_t)stream));
+}
+
+int hobflops_unpack(const uint32_t* planes, int64_t rows, int64_t len, hobflops_fmt f, int kind,
+                    void* dst, void* stream) {
+  if (rows < 0 || len < 0 || !fmt_ok(f)) return HOBFLOPS_EINVAL;
+  if (kind != HOBFLOPS_SRC_F32 && kind != HOBFLOPS_SRC_CODE_U32) return HOBFLOPS_EINVAL;
+  if (rows == 0 || len == 0) return HOBFLOPS_OK;
+  if (!dst || !planes) return HOBFLOPS_EINVAL;
+  if (!aligned(dst) || !aligned(planes)) return HOBFLOPS_EALIGN;
+  if ((len + 31) / 32 > INT32_MAX) return HOBFLOPS_EINVAL;
+  return hip_status(launch_unpack(planes, rows, len, f.wE, f.wF, kind, dst, (hipStream_t)stream));
+}
+
+int hobflops_conv2d_supported(const hobflops_conv_desc* d) {
+  return conv_check(d) == HOBFLOPS_OK && find_conv(d) != nullptr;
+}
+
+int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
+                    const hobflops_conv_desc* d, void* stream) {
+  const int st = conv_check(d);
+  if (st != HOBFLOPS_OK) return st;
+  if (!ifm || !w || !ofm) return HOBFLOPS_EINVAL;
+  if (!aligned(ifm) || !aligned(w) || !aligned(ofm)) return HOBFLOPS_EALIGN;
+  const ConvVariant* v = find_conv(d);
+  if (!v) return HOBFLOPS_EUNSUPPORTED;
+  ConvParams p;
+  p.N = d->N;
+  p.H = d->H;
+  p.W = d->W;
+  p.C = d->C;
+  p.M = d->M;
+  p.KH = d->KH;
+  p.KW = d->KW;
+  p.stride = d->stride;
+  p.pad = d->pad;
+  p.OH = (d->H + 2 * d->pad - d->KH) / d->stride + 1;
+  p.OW = (d->W + 2 * d->pad - d->KW) / d->stride + 1;
+  p.CG = (d->C + 31) / 32;
+  p.MT = (d->M + 31) / 32;
+  p.P = p.N * p.OH * p.OW;
+  int algo = d->algo;
+  if (algo == HOBFLOPS_ALGO_AUTO) {
+    // one accumulator wave per 64 positions and m-tile; split when they would
+    // leave the SIMDs of the device at most one each
+    int dev = 0, cus = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_status(e);
+    const int64_t chain_waves = (int64_t)((p.P + 63) / 64) * p.MT;
+    algo = chain_waves <= 4 * (int64_t)cus ? HOBFLOPS_ALGO_SPLIT : HOBFLOPS_ALGO_FUSED;
+  }
+  return hip_status(v->launch(ifm, w, ofm, p, algo == HOBFLOPS_ALGO_SPLIT ? kAlgoSplit : kAlgoFused,
+                              (hipStream_t)stream));
+}
+
+int hobflops_muladd_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt) {
+  return fmt_ok(in_fmt) && fmt_ok(acc_fmt) && find_muladd(in_fmt, acc_fmt) != nullptr;
+}
+
+int hobflops_muladd(const uint32_t* a, const uint32_t* b, const uint32_t* c, uint32_t* r,
+                    int64_t n, hobflops_fmt in_fmt, hobflops_fmt acc_fmt, void* stream) {
+  if (n < 0 || !fmt_ok(in_fmt) || !fmt_ok(acc_fmt)) return HOBFLOPS_EINVAL;
+  if (acc_fmt.wE != in_fmt.wE || acc_fmt.wF < in_fmt.wF) return HOBFLOPS_EINVAL;
+  const MuladdVariant* v = find_muladd(in_fmt, acc_fmt);
+  if (!v) return HOBFLOPS_EUNSUPPORTED;
+  if (n == 0) return HOBFLOPS_OK;
+  if (!a || !b || !c || !r) return HOBFLOPS_EINVAL;
+  if (!aligned(a) || !aligned(b) || !aligned(c) || !aligned(r)) return HOBFLOPS_EALIGN;
+  return hip_status(v->launch(a, b, c, r, (n + 31) / 32, (hipStream_t)stream));
+}
+
+int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int* conv_mac_ops,
+                         int* conv_mul_ops, int* conv_accum_ops, int* muladd_ops) {
+  int found = 0;
+  if (conv_mac_ops) *conv_mac_ops = 0;
+  if (conv_mul_ops) *conv_mul_ops = 0;
+  if (conv_accum_ops) *conv_accum_ops = 0;
+  if (muladd_ops) *muladd_ops = 0;
+  for (int i = 0; i < kNumConvVariants; ++i) {
+    const ConvVariant& v = kConvVariants[i];
+    if (v.wE == in_fmt.wE && v.wF_in == in_fmt.wF && v.wF_acc == acc_fmt.wF &&
+        acc_fmt.wE == in_fmt.wE) {
+      if (conv_mac_ops) *conv_mac_ops = v.mac_ops;
+      if (conv_mul_ops) *conv_mul_ops = v.mul_ops;
+      if (conv_accum_ops) *conv_accum_ops = v.accum_ops;
+      found = 1;
+      break;
+    }
+  }
+  const MuladdVariant* m = find_muladd(in_fmt, acc_fmt);
+  if (m) {
+    if (muladd_ops) *muladd_ops = m->ops;
+    found = 1;
+  }
+  return found ? HOBFLOPS_OK : HOBFLOPS_EUNSUPPORTED;
+}
+
+const char* hobflops_status_string(int status) {
+  switch (status) {
+    case HOBFLOPS_OK: return "ok";
+    case HOBFLOPS_EINVAL: return "invalid argument";
+    case HOBFLOPS_EUNSUPPORTED: return "no generated kernel for this format combination";
+    case HOBFLOPS_EALIGN: return "pointer not 4-byte aligned";
+    case HOBFLOPS_EHIP: return g_errbuf[0] ? g_errbuf : "HIP error";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

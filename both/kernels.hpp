@@ -1,0 +1,388 @@
+// Bitsliced HOBFLOPS kernels for gfx950 (templates over a generated variant).
+//
+// Plane layout (PL32): a packed tensor with logical shape [R][L], packed
+// along L, is stored as uint32 words[R][ceil(L/32)][NB]; bit j of
+// words[r][g][b] is bit b of the code at (r, 32g + j). Padding lanes hold
+// code 0 (+0). This is the bitslice-parallel layout of the paper (Sec. 3.2,
+// "many values transformed" figure) with 32-lane words.
+//
+// A Variant type supplies the generated netlists:
+//   static constexpr int NIN, NACC, NOUT;     planes per value
+//   static __device__ void mac(uint32_t (&acc)[NACC], const uint32_t (&w)[NIN],
+//                              const uint32_t (&x)[NIN]);        acc = acc + w*x
+//   static __device__ void epi(const uint32_t (&acc)[NACC], uint32_t (&out)[NOUT]);
+// or, for the element-wise kernel,
+//   static __device__ void muladd(const uint32_t (&a)[NIN], const uint32_t (&b)[NIN],
+//                                 const uint32_t (&c)[NIN], uint32_t (&r)[NACC]);
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hobflops {
+
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
+
+struct ConvParams {
+  int N, H, W, C, M, KH, KW, stride, pad;
+  int OH, OW;
+  int CG;  // ceil(C / 32): channel words per IFM position
+  int MT;  // ceil(M / 32): kernel words (m-tiles) per weight row / OFM position
+  int P;   // N * OH * OW output positions
+};
+
+constexpr int kConvBlock = 256;  // positions per workgroup: four wave64s
+
+// Kernel shapes of the convolution (hobflops_conv_desc.algo).
+constexpr int kAlgoAuto = 0, kAlgoFused = 1, kAlgoSplit = 2;
+
+
+// MCMK convolution (paper Sec. 3.4). One lane owns one output position and
+// one m-tile of 32 kernels, so every VALU bitwise instruction of the MAC
+// netlist performs 32 MACs. A workgroup's four waves cover 256 consecutive
+// positions of one m-tile: the 32-kernel weight word of a tap is the same for
+// all of them, while each lane broadcasts its own IFM value's bits into
+// all-zero / all-one words (the paper broadcasts the IFM channel value across
+// the kernel lanes). For every output the accumulator planes stay in VGPRs and
+// the taps are taken in the fixed order ky, kx, c; a padding tap contributes
+// x = +0.
+//
+// Work is walked in chunks (ky, kx, 32-channel word). With one wave per SIMD
+// nothing hides memory latency, so operands are fetched one step ahead:
+//  - the weight rows of the next chunk (at most 32 rows of NIN words, one
+//    per channel) are loaded from HBM into registers while the current chunk
+//    runs, then written to the other half of a double-buffered LDS tile
+//    shared by the workgroup; each MAC reads its row with 16-byte LDS loads
+//    (one address for the whole wave: a broadcast), prefetched one row ahead;
+//  - each lane's IFM channel word of the next chunk is loaded while the
+//    current chunk's channels are processed.
+// Prefetch addresses are clamped into the buffers, so no load is out of
+// bounds, and every lane of the workgroup takes part in the staging.
+template <class V>
+__global__ __launch_bounds__(kConvBlock) void conv2d_kernel(const uint32_t* __restrict__ ifm,
+                                                            const uint32_t* __restrict__ w,
+                                                            uint32_t* __restrict__ ofm,
+                                                            ConvParams p) {
+  constexpr int NIN = V::NIN, NACC = V::NACC, NOUT = V::NOUT;
+  constexpr int NINP = (NIN + 3) & ~3;  // LDS row stride: rows start 16-byte aligned
+  constexpr int kRows = 32;             // weight rows per chunk (one channel word)
+  constexpr int kStage = (kRows * NIN + kConvBlock - 1) / kConvBlock;
+  __shared__ uint4 wtile[2][kRows * NINP / 4];
+
+  const int tid = threadIdx.x;
+  const int mt = blockIdx.y;
+  const int pos = blockIdx.x * kConvBlock + tid;
+  const bool active = pos < p.P;
+  const int q = active ? pos : 0;
+  const int ox = q % p.OW;
+  const int oy = (q / p.OW) % p.OH;
+  const int n = q / (p.OW * p.OH);
+  const int iy0 = oy * p.stride - p.pad, ix0 = ox * p.stride - p.pad;
+  const uint32_t* img = ifm + (size_t)n * p.H * p.W * p.CG * NIN;
+  const size_t wrow = (size_t)p.MT * NIN;  // words between consecutive weight rows
+  const uint32_t* wm = w + (size_t)mt * NIN;
+
+  // Raw IFM words of chunk (ky, kx, cg) for this lane; *valid is false for a
+  // padding tap (the words then come from a clamped, in-bounds address and are
+  // replaced by zero, i.e. +0, only when the chunk is used, so that the load's
+  // latency is not waited for here).
+  auto load_ifm = [&](int ky, int kx, int cg, uint32_t(&xw)[NIN], bool* valid) {
+    const int iy = iy0 + ky, ix = ix0 + kx;
+    *valid = active && iy >= 0 && iy < p.H && ix >= 0 && ix < p.W;
+    const uint32_t* ip =
+        img + (((size_t)(*valid ? iy : 0) * p.W + (*valid ? ix : 0)) * p.CG + cg) * NIN;
+#pragma unroll
+    for (int b = 0; b < NIN; ++b) xw[b] = ip[b];
+  };
+  // This thread's share of the weight rows r0 .. r0+nc-1 (HBM -> registers).
+  uint32_t stage[kStage];
+  auto fetch_w = [&](int r0, int nc) {
+#pragma unroll
+    for (int s = 0; s < kStage; ++s) {
+      const int i = tid + s * kConvBlock;
+      const int row = i / NIN, b = i - (i / NIN) * NIN;
+      const int r = (row < nc && i < kRows * NIN) ? r0 + row : r0;
+      stage[s] = wm[(size_t)r * wrow + (row < nc ? b : 0)];
+    }
+  };
+  auto store_w = [&](int buf) {
+    uint32_t* t = reinterpret_cast<uint32_t*>(wtile[buf]);
+#pragma unroll
+    for (int s = 0; s < kStage; ++s) {
+      const int i = tid + s * kConvBlock;
+      if (i < kRows * NIN) t[(i / NIN) * NINP + (i - (i / NIN) * NIN)] = stage[s];
+    }
+  };
+  auto read_row = [&](int buf, int c, uint32_t(&wv)[NIN]) {
+    const uint32_t* t = reinterpret_cast<const uint32_t*>(wtile[buf]) + c * NINP;
+#pragma unroll
+    for (int b = 0; b < NIN; ++b) wv[b] = t[b];
+  };
+
+  uint32_t acc[NACC];
+#pragma unroll
+  for (int b = 0; b < NACC; ++b) acc[b] = 0u;  // +0
+
+  uint32_t xn[NIN];
+  bool xn_valid;
+  fetch_w(0, min(kRows, p.C));
+  load_ifm(0, 0, 0, xn, &xn_valid);
+  store_w(0);
+  __syncthreads();
+
+  int ky = 0, kx = 0, cg = 0;
+  const int nchunks = p.KH * p.KW * p.CG;
+  for (int ch = 0; ch < nchunks; ++ch) {
+    const int buf = ch & 1;
+    const int nc = min(kRows, p.C - kRows * cg);
+    int cg2 = cg + 1, kx2 = kx, ky2 = ky;
+    if (cg2 == p.CG) {
+      cg2 = 0;
+      if (++kx2 == p.KW) {
+        kx2 = 0;
+        if (++ky2 == p.KH) ky2 = 0;  // past the end: refetch chunk 0, unused
+      }
+    }
+    uint32_t xw[NIN];
+#pragma unroll
+    for (int b = 0; b < NIN; ++b) xw[b] = xn_valid ? xn[b] : 0u;
+    fetch_w((ky2 * p.KW + kx2) * p.C + kRows * cg2, min(kRows, p.C - kRows * cg2));
+    load_ifm(ky2, kx2, cg2, xn, &xn_valid);
+
+    // Two rows in flight, ping-pong: the next row's LDS loads are issued
+    // before the current MAC, and a scheduling barrier keeps them there (the
+    // scheduler would otherwise sink them next to their use).
+    auto mac_step = [&](const uint32_t(&wv)[NIN], int c) {
+      uint32_t x[NIN];
+#pragma unroll
+      for (int b = 0; b < NIN; ++b)
+        x[b] = (uint32_t)__builtin_amdgcn_sbfe((int)xw[b], c, 1);  // bit c -> 0 / ~0
+      V::mac(acc, wv, x);
+    };
+    uint32_t wa[NIN], wb[NIN];
+    read_row(buf, 0, wa);
+    int c = 0;
+    for (; c + 2 <= nc; c += 2) {
+      read_row(buf, c + 1, wb);
+      __builtin_amdgcn_sched_barrier(0);
+      mac_step(wa, c);
+      read_row(buf, c + 2 < nc ? c + 2 : c + 1, wa);
+      __builtin_amdgcn_sched_barrier(0);
+      mac_step(wb, c + 1);
+    }
+    if (c < nc) mac_step(wa, c);
+    store_w(buf ^ 1);
+    __syncthreads();
+    cg = cg2;
+    kx = kx2;
+    ky = ky2;
+  }
+  if (!active) return;
+  uint32_t out[NOUT];
+  V::epi(acc, out);
+  uint32_t* op = ofm + ((size_t)pos * p.MT + mt) * NOUT;
+#pragma unroll
+  for (int b = 0; b < NOUT; ++b) op[b] = out[b];
+}
+
+// MCMK convolution, split shape: multiply and accumulate on different waves.
+//
+// A wave issues at most one instruction every four clocks, half of what its
+// SIMD's VALU can retire, and the chain of adds into one accumulator cannot be
+// reordered (the fixed accumulation order), so a launch with about one chain
+// wave per SIMD leaves half of the VALU idle. The products w*x do not depend
+// on the accumulator, so here each workgroup runs 4 accumulator waves (waves
+// 0-3: 64 positions each, one m-tile, accumulator planes in VGPRs, the adder
+// netlist only) and 4 multiplier waves (waves 4-7: the same positions; IFM bit
+// broadcast and the multiplier netlist). Both netlists run as inline assembly
+// whose registers avoid VGPR bank conflicts, so that two waves on a SIMD both
+// issue at full rate.
+//
+// Taps are processed in batches of V::kBatch (even) in the fixed tap order.
+// In iteration b, between two workgroup barriers:
+//  - accumulator wave i adds the products of batch b (LDS product ring, half b%2);
+//  - multiplier wave 4+i computes the products of batch b+1 into half (b+1)%2,
+//    reading the batch's weight rows from LDS weight-ring slot (b+1)%3; a tap
+//    past the end gets the product -0, which leaves every accumulator value
+//    unchanged (x + -0 = x for all x, including both zeros);
+//  - the multiplier waves together load the weight rows of batch b+2 from HBM
+//    (one word per thread) and store them into weight-ring slot (b+2)%3.
+// Each ring slot written in iteration b was last read in iteration b-1 or
+// b-2, before a barrier, and is read only after the barrier that ends b.
+// Every wave reaches every barrier, so the loop cannot deadlock.
+template <class V>
+__global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
+    const uint32_t* __restrict__ ifm, const uint32_t* __restrict__ w, uint32_t* __restrict__ ofm,
+    ConvParams p) {
+  constexpr int NIN = V::NIN, NACC = V::NACC, NOUT = V::NOUT;
+  constexpr int NINP = (NIN + 3) & ~3;    // weight row stride in LDS (16-byte aligned)
+  constexpr int NACCP = (NACC + 3) & ~3;  // product entry per lane (16-byte aligned)
+  constexpr int K = V::kBatch;
+  constexpr int kStride = NACCP / 4;  // uint4 per product entry
+  static_assert(K % 2 == 0, "the accumulator ping-pong needs an even batch");
+  static_assert(K * NIN <= kConvBlock, "one weight word per multiplier thread");
+  static_assert(2 * K * 256 * NACCP * 4 <= 128 * 1024, "product ring exceeds the LDS budget");
+  __shared__ uint4 pring[2 * K * 4 * 64 * kStride];  // [half][k][wave][lane][kStride]
+  __shared__ uint4 wring[3 * K * NINP / 4];          // [slot][k][NINP words]
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const bool mul_role = wave >= 4;
+  const int pw = wave & 3;
+  const int mt = blockIdx.y;
+  const int pos = blockIdx.x * kConvBlock + pw * 64 + lane;
+  const bool active = pos < p.P;
+  const int q = active ? pos : 0;
+  const int ox = q % p.OW;
+  const int oy = (q / p.OW) % p.OH;
+  const int n = q / (p.OW * p.OH);
+  const int iy0 = oy * p.stride - p.pad, ix0 = ox * p.stride - p.pad;
+  const uint32_t* img = ifm + (size_t)n * p.H * p.W * p.CG * NIN;
+  const size_t wrow = (size_t)p.MT * NIN;
+  const uint32_t* wm = w + (size_t)mt * NIN;
+  const int T = p.KH * p.KW * p.C;  // taps per output
+  const int nb = (T + K - 1) / K;
+
+  auto entry = [&](int b, int k) {
+    // C-style cast: generic pointer into the LDS address space
+    return (lds_u32*)(pring + ((((size_t)(b & 1) * K + k) * 4 + pw) * 64 + lane) * kStride);
+  };
+
+  // ---- multiplier waves: weight staging (thread t of the 256 loads word t)
+  const int mt_tid = threadIdx.x - 4 * 64;
+  uint32_t wstage = 0;
+  auto fetch_w = [&](int b) {  // HBM -> register, rows of batch b (clamped)
+    if (mt_tid < K * NIN) {
+      const int k = mt_tid / NIN, bb = mt_tid - (mt_tid / NIN) * NIN;
+      const int t = min(b * K + k, T - 1);
+      wstage = wm[(size_t)t * wrow + bb];
+    }
+  };
+  auto store_w = [&](int b) {
+    if (mt_tid < K * NIN) {
+      const int k = mt_tid / NIN, bb = mt_tid - (mt_tid / NIN) * NIN;
+      reinterpret_cast<uint32_t*>(wring)[((b % 3) * K + k) * NINP + V::kWSlot[bb]] = wstage;
+    }
+  };
+
+  // ---- multiplier waves: IFM words of the current and the next chunk
+  uint32_t xw[NIN], xn[NIN];
+  bool xn_valid = false;          // xn is a real tap (else the chunk reads as +0)
+  int nky = 0, nkx = 0, ncg = 0;  // coordinates of the chunk held in xn
+  int c = 0, nc = 0;              // channel within the current chunk, its size
+  auto load_ifm = [&](int ky, int kx, int cg) {  // raw words; masked when used
+    const int iy = iy0 + ky, ix = ix0 + kx;
+    xn_valid = active && iy >= 0 && iy < p.H && ix >= 0 && ix < p.W;
+    const uint32_t* ip =
+        img + (((size_t)(xn_valid ? iy : 0) * p.W + (xn_valid ? ix : 0)) * p.CG + cg) * NIN;
+#pragma unroll
+    for (int b = 0; b < NIN; ++b) xn[b] = ip[b];
+  };
+  auto advance = [&]() {  // move to the next (ky, kx, channel-word) chunk
+#pragma unroll
+    for (int bb = 0; bb < NIN; ++bb) xw[bb] = xn_valid ? xn[bb] : 0u;
+    nc = min(32, p.C - 32 * ncg);
+    c = 0;
+    if (++ncg == p.CG) {
+      ncg = 0;
+      if (++nkx == p.KW) {
+        nkx = 0;
+        if (++nky == p.KH) nky = 0;  // past the end: chunk 0 again, unused
+      }
+    }
+    load_ifm(nky, nkx, ncg);
+  };
+  auto produce = [&](int b) {
+    const int t0 = b * K;
+    const int tk = min(K, T - t0);
+    const lds_u32* wr = (const lds_u32*)wring + (b % 3) * K * NINP;
+    if (c == nc) advance();
+    if (tk == K && c + K <= nc) {  // whole batch inside one channel word
+      V::product_batch(xw, c, wr, entry(b, 0));
+      c += K;
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // products visible at the barrier
+      return;
+    }
+#pragma unroll
+    for (int k = 0; k < K; ++k) {
+      if (k < tk) {
+        if (c == nc) advance();
+        V::product_step(xw, c, wr + k * NINP, entry(b, k));
+        ++c;
+      } else {  // tap past the end: product -0 (the sign plane all ones)
+        lds_u32* e = entry(b, k);
+#pragma unroll
+        for (int bb = 0; bb < NACCP; ++bb) e[bb] = 0u;
+        e[V::kProdSlot[NACC - 3]] = 0xFFFFFFFFu;
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // products visible at the barrier
+  };
+
+  // ---- accumulator waves: planes in register-slot order (V::kAccSlot)
+  uint32_t acc[NACCP];
+#pragma unroll
+  for (int s = 0; s < NACCP; ++s) acc[s] = 0u;  // +0
+
+  // Each role runs its own loop with the same number of barriers (nb + 2),
+  // so that the multiplier's register use never meets the accumulator's
+  // loop-carried planes. The accumulator waves issue at raised priority: they
+  // carry the serial chain, the multiplier waves fill the issue slots left.
+  if (mul_role) {
+    // prologue: weights of batches 0 and 1 staged, products of batch 0 made
+    load_ifm(0, 0, 0);
+    fetch_w(0);
+    store_w(0);
+    fetch_w(1);
+    store_w(1);
+    __syncthreads();
+    fetch_w(2);
+    produce(0);
+    store_w(2);
+    __syncthreads();
+    for (int b = 0; b < nb; ++b) {
+      fetch_w(b + 3);
+      if (b + 1 < nb) produce(b + 1);
+      store_w(b + 3);
+      __syncthreads();
+    }
+    return;
+  }
+  __builtin_amdgcn_s_setprio(3);
+  __syncthreads();
+  __syncthreads();
+  for (int b = 0; b < nb; ++b) {
+    V::accum_batch(acc, entry(b, 0));
+    __syncthreads();
+  }
+  if (!active) return;
+  uint32_t planes[NACC], out[NOUT];
+#pragma unroll
+  for (int bb = 0; bb < NACC; ++bb) planes[bb] = acc[V::kAccSlot[bb]];
+  V::epi(planes, out);
+  uint32_t* op = ofm + ((size_t)pos * p.MT + mt) * NOUT;
+#pragma unroll
+  for (int bb = 0; bb < NOUT; ++bb) op[bb] = out[bb];
+}
+
+// Element-wise r = a*b + c (multiply rounded, then add rounded) on flat PL32
+// tensors: one lane owns one word group, i.e. 32 independent triples.
+template <class V>
+__global__ __launch_bounds__(256) void muladd_kernel(const uint32_t* __restrict__ a,
+                                                     const uint32_t* __restrict__ b,
+                                                     const uint32_t* __restrict__ c,
+                                                     uint32_t* __restrict__ r, int64_t groups) {
+  constexpr int NIN = V::NIN, NACC = V::NACC;
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= groups) return;
+  uint32_t av[NIN], bv[NIN], cv[NIN], rv[NACC];
+#pragma unroll
+  for (int i = 0; i < NIN; ++i) {
+    av[i] = a[g * NIN + i];
+    bv[i] = b[g * NIN + i];
+    cv[i] = c[g * NIN + i];
+  }
+  V::muladd(av, bv, cv, rv);
+#pragma unroll
+  for (int i = 0; i < NACC; ++i) r[g * NACC + i] = rv[i];
+}
+
+}  // namespace hobflops
