@@ -78,9 +78,9 @@ def netlist(kind, key, cache):
 
 
 def split_batch(naccp):
-    """Products per barrier in the split kernel (even; the LDS ring of
-    2 x batch x 256 lanes x entry words must stay within 128 KiB)."""
-    return 4 if naccp <= 16 else 2
+    """Products per barrier in the split kernel: even, and the LDS product
+    ring of 2 halves x batch x 256 lanes x entry words within 128 KiB."""
+    return 4 if 2 * 4 * 256 * naccp * 4 <= 128 * 1024 else 2
 
 
 def split_asm(wE, wi, wa, cache):
@@ -130,9 +130,9 @@ struct V {{
   static constexpr const int* kAccSlot = conv_{tag}::kAccSlot;
   static constexpr const int* kProdSlot = conv_{tag}::kProdSlot;
   static constexpr const int* kWSlot = conv_{tag}::kWSlot;
-  static __device__ __forceinline__ void accum_batch(uint32_t (&acc)[(NACC + 3) & ~3],
-                                                     const lds_u32* entry) {{
-    conv_{tag}::accum_batch(acc, entry);
+  static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[(NACC + 3) & ~3],
+                                                    const lds_u32* e0, const lds_u32* e1, int nb) {{
+    conv_{tag}::accum_loop(acc, e0, e1, nb);
   }}
   static __device__ __forceinline__ void product_step(const uint32_t (&xw)[NIN], int c,
                                                       const lds_u32* wrow, lds_u32* entry) {{

@@ -241,7 +241,7 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   const int T = p.KH * p.KW * p.C;  // taps per output
   const int nb = (T + K - 1) / K;
 
-  auto entry = [&](int b, int k) {
+  auto entry = [&](int b, int k) {  // batch b lives in ring half b % 2
     // C-style cast: generic pointer into the LDS address space
     return (lds_u32*)(pring + ((((size_t)(b & 1) * K + k) * 4 + pw) * 64 + lane) * kStride);
   };
@@ -322,6 +322,11 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
 #pragma unroll
   for (int s = 0; s < NACCP; ++s) acc[s] = 0u;  // +0
 
+  // Schedule, one barrier per step i = -1 .. nb-1: the multiplier waves make
+  // batch i+1 (into ring half (i+1) % 2) and stage the weights of batch i+3
+  // (into weight slot i % 3, last read at step i-2); the accumulator waves add
+  // batch i, complete since the barrier of step i-1. Half i % 2 is rewritten
+  // at step i+1, after the accumulators' last read of it.
   // Each role runs its own loop with the same number of barriers (nb + 2),
   // so that the multiplier's register use never meets the accumulator's
   // loop-carried planes. The multiplier waves issue at raised priority: their
@@ -331,31 +336,23 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   // single-wave rate either way.
   if (mul_role) {
     __builtin_amdgcn_s_setprio(3);
-    // prologue: weights of batches 0 and 1 staged, products of batch 0 made
     load_ifm(0, 0, 0);
     fetch_w(0);
     store_w(0);
     fetch_w(1);
     store_w(1);
     __syncthreads();
-    fetch_w(2);
-    produce(0);
-    store_w(2);
-    __syncthreads();
-    for (int b = 0; b < nb; ++b) {
-      fetch_w(b + 3);
-      if (b + 1 < nb) produce(b + 1);
-      store_w(b + 3);
+    for (int i = -1; i < nb; ++i) {
+      fetch_w(i + 3);
+      if (i + 1 < nb) produce(i + 1);
+      store_w(i + 3);
       __syncthreads();
     }
     return;
   }
   __syncthreads();
   __syncthreads();
-  for (int b = 0; b < nb; ++b) {
-    V::accum_batch(acc, entry(b, 0));
-    __syncthreads();
-  }
+  V::accum_loop(acc, entry(0, 0), entry(1, 0), nb);  // nb barriers
   if (!active) return;
   uint32_t planes[NACC], out[NOUT];
 #pragma unroll

@@ -4,12 +4,16 @@ The two wave roles of the split kernel run their netlists as inline assembly
 with explicit registers chosen by gen.regalloc, so that no VALU instruction
 reads two VGPRs of one bank (see gen/regalloc.py). The functions produced:
 
-* ``accum_batch(acc, entry)``: reads the products of one batch (K entries of
-  the LDS product ring, 16-byte loads at immediate offsets from this lane's
-  first entry) and adds them into the accumulator with K copies of the adder
-  netlist; the accumulator ping-pongs between two register sets and is back in
-  the first after the batch (K is even). ``acc`` holds the accumulator planes
-  in register-slot order; kAccSlot[b] is the slot of plane b.
+* ``accum_loop(acc, e0, e1, nb)``: the whole accumulator role. Batch b (K
+  products) sits in half b % 2 of the LDS product ring; after each barrier
+  the K entries are requested with 16-byte loads at immediate offsets from
+  this lane's first entry, and K copies of the adder netlist add them into the
+  accumulator, each waiting for its own entry only. The accumulator
+  ping-pongs between two register sets and is back in the first after the
+  batch (K is even). ``acc`` holds the accumulator planes in register-slot
+  order; kAccSlot[b] is the slot of plane b. (Requesting the next batch's
+  entries before the barrier, from a third ring slot, was measured slower:
+  the early loads compete with the multiplier's stores.)
 * ``product_batch(xw, c, wrow, entry)``: the K products of one batch whose
   taps c .. c+K-1 lie in one IFM channel word: all K weight rows are requested
   from the LDS weight ring first (plane b in word kWSlot[b]); per product, bit
@@ -61,31 +65,48 @@ def split_functions(accum_C, prod_C, nin, nacc, K):
     acc_slot = [r - BASE for r in place["in"]["acc"]]
     prod_slot = [r - P[0][0] for r in place["in"]["p"]]
     entry_bytes = 4 * 64 * kstride * 16  # ring distance between batch entries k and k+1
-    body = ["s_waitcnt lgkmcnt(0)"]
-    for k in range(K):
-        for j in range(kstride):
-            r0 = P[k][4 * j]
-            body.append(f"ds_read_b128 v[{r0}:{r0 + 3}], %[e] offset:{k * entry_bytes + 16 * j}")
-    for k in range(K):
-        body.append(f"s_waitcnt lgkmcnt({(K - 1 - k) * kstride})")
-        m = {}
-        if k % 2 == 1:  # B -> A
-            m.update({a: b for a, b in zip(A, B)})
-            m.update({b: a for a, b in zip(A, B)})
-        m.update({p0: pk for p0, pk in zip(P[0], P[k])})
-        body += _rename(lines, m)
+
+    def batch(half):
+        """One batch from ring half `half`: all K entries are requested after
+        the barrier, and the adder for entry k waits for entry k only."""
+        out = [f"ds_read_b128 v[{P[k][4 * j]}:{P[k][4 * j] + 3}], %[e{half}] "
+               f"offset:{k * entry_bytes + 16 * j}" for k in range(K) for j in range(kstride)]
+        for k in range(K):
+            out.append(f"s_waitcnt lgkmcnt({(K - 1 - k) * kstride})")
+            m = {}
+            if k % 2 == 1:  # B -> A
+                m.update({a: b for a, b in zip(A, B)})
+                m.update({b: a for a, b in zip(A, B)})
+            m.update({p0: pk for p0, pk in zip(P[0], P[k])})
+            out += _rename(lines, m)
+        return out
+
+    # A barrier ends each batch. The count is exact: the loop starts with
+    # nothing of the compiler's in flight and ends with nothing of its own.
+    body = ["s_waitcnt lgkmcnt(0)", "s_mov_b32 %[n], %[nb]", "L%=_loop:"]
+    for half in range(2):
+        body += batch(half)
+        body += ["s_barrier",
+                 "s_sub_u32 %[n], %[n], 1",
+                 "s_cmp_eq_u32 %[n], 0",
+                 "s_cbranch_scc1 L%=_done"]
+    body += ["s_branch L%=_loop", "L%=_done:"]
     used = set(B) | set(r for blk in P for r in blk) | set(st_acc["temps"])
     clob = ", ".join(f'"v{r}"' for r in sorted(used))
     state = ", ".join(f'"+{{v{BASE + s}}}"(acc[{s}])' for s in range(naccp))
     accum_fn = f"""static constexpr int kAccSlot[{nacc}] = {{{", ".join(map(str, acc_slot))}}};
 static constexpr int kProdSlot[{nacc}] = {{{", ".join(map(str, prod_slot))}}};
-// Adds the K products of one batch into acc (planes in register-slot order).
-static __device__ __forceinline__ void accum_batch(uint32_t (&acc)[{naccp}], const lds_u32* entry) {{
+// The accumulator role: nb batches of K products from the two-half LDS ring
+// (this lane's first entry of half h at e_h, batch b in half b % 2), one
+// barrier after each batch; acc holds the planes in register-slot order.
+static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], const lds_u32* e0,
+                                                  const lds_u32* e1, int nb) {{
+  uint32_t n;
   asm volatile(
 {_asm_string(body)}
-      : {state}
-      : [e] "v"(entry)
-      : {clob}, "memory");
+      : {state}, [n] "=&s"(n)
+      : [e0] "v"(e0), [e1] "v"(e1), [nb] "s"(nb)
+      : {clob}, "scc", "memory");
 }}
 """
     # ---- multiplier role: product planes go to the P block in slot order
