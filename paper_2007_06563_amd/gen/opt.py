@@ -13,9 +13,11 @@ one instruction (gfx950 ``v_bitop3_b32``):
   same cut is replaced by that signal;
 * area-oriented cut mapping with exact-area recovery: choose one cut per
   mapped node so that the number of LUTs is smallest;
-* resynthesis of small windows: a node whose function over up to five inputs
-  admits a cheaper two- or three-LUT decomposition than its current cone gets
-  that decomposition.
+* resynthesis of small windows: a node whose function over a cut of four or
+  five signals can be written as g(h(S), T) -- two LUTs, h over at most three
+  of the signals and g over h and the other (at most two) -- while the part
+  of its cone that nothing else uses holds more than two LUTs, gets that
+  decomposition.
 """
 import itertools
 
@@ -251,16 +253,146 @@ def lut_map(C: Circuit, rounds=3):
     return rebuild(C, cover=cover)
 
 
+def _cofactor2(tt, k, i, vi, j, vj):
+    """tt (k inputs) with inputs i < j fixed; the result is over the rest, in order."""
+    return tt_cofactor(tt_cofactor(tt, k, j, vj), k - 1, i, vi)
+
+
+def decompose2(tt, k):
+    """f = g(h(S), T) for a k-input function (k = 4 or 5) whose inputs are all
+    essential: T two inputs, S the other inputs, for k = 4 possibly with one
+    input of T added. Returns (S, h_tt, T, g_tt), S and T as input indices
+    (g's inputs are h, T[0], T[1]), or None."""
+    for T in itertools.combinations(range(k), 2):
+        R = [v for v in range(k) if v not in T]
+        m = len(R)
+        full = tt_mask(m)
+        cof = [_cofactor2(tt, k, T[0], a & 1, T[1], a >> 1) for a in range(4)]
+        # the non-constant cofactors, grouped by the value of the input of T
+        # that h may also read (None: h reads R only)
+        for shared in [None] + ([0, 1] if k == 4 else []):
+            hs, kinds, ok = {}, [], True
+            for a in range(4):
+                c = cof[a]
+                if c in (0, full):
+                    kinds.append(c & 1)
+                    continue
+                key = None if shared is None else (a >> shared) & 1
+                h = hs.setdefault(key, c)
+                if c == h:
+                    kinds.append("h")
+                elif c == ~h & full:
+                    kinds.append("~h")
+                else:
+                    ok = False
+                    break
+            if not ok or not hs:
+                continue
+            if shared is None:
+                S, h_tt = R, next(iter(hs.values()))
+            else:
+                t = T[shared]
+                S = sorted(R + [t])
+                h_tt = 0
+                for idx in range(8):
+                    bits = {S[i]: (idx >> i) & 1 for i in range(3)}
+                    r_idx = sum(bits[r] << i for i, r in enumerate(R))
+                    h = hs.get(bits[t], 0)
+                    h_tt |= ((h >> r_idx) & 1) << idx
+            g_tt = 0
+            for a in range(4):
+                for hv in (0, 1):
+                    kind = kinds[a]
+                    out = hv if kind == "h" else (1 - hv if kind == "~h" else kind)
+                    g_tt |= out << (hv | (a << 1))
+            return list(S), h_tt, list(T), g_tt
+    return None
+
+
+def _mffc_size(C, n, leaves, fanout):
+    """LUTs of n's cone above `leaves` that no node outside the cone uses."""
+    refs = {}
+    stop = set(leaves)
+    count, stack = 0, [n]
+    while stack:
+        m = stack.pop()
+        count += 1
+        for f in C.fanins[m]:
+            if f in stop or C.is_input[f] or f == 0:
+                continue
+            refs[f] = refs.get(f, 0) + 1
+            if refs[f] == fanout[f]:
+                stack.append(f)
+    return count
+
+
+def resynthesize(C: Circuit, max_steps=10000):
+    """Apply the best two-LUT window decomposition (see decompose2) while
+    one saves a LUT."""
+    memo = {}
+    for _ in range(max_steps):
+        cuts = enumerate_cuts(C, k=5, limit=40)
+        N = len(C.fanins)
+        fanout = [0] * N
+        for m in range(1, N):
+            for f in C.fanins[m]:
+                fanout[f] += 1
+        for _, lits in C.outputs:
+            for l in lits:
+                fanout[l >> 1] += 1
+        cands = []
+        for n in range(1, N):
+            if C.is_input[n]:
+                continue
+            for leaves, tt in cuts[n][:-1]:
+                if len(leaves) < 4:
+                    continue
+                key = (tt, len(leaves))
+                if key not in memo:
+                    memo[key] = decompose2(tt, len(leaves))
+                d = memo[key]
+                if d is None:
+                    continue
+                gain = _mffc_size(C, n, leaves, fanout) - 2
+                if gain > 0:
+                    cands.append((gain, n, leaves, d))
+        applied = False
+        for gain, n, leaves, (S, h_tt, T, g_tt) in sorted(cands, key=lambda c: -c[0]):
+            D = Circuit(C.name)
+            m = {0: 0}
+            for group, lits in C.inputs:
+                for l, nl in zip(lits, D.input(group, len(lits))):
+                    m[l >> 1] = nl
+            for v in range(1, N):
+                if C.is_input[v]:
+                    continue
+                if v == n:
+                    h = D.lut(h_tt, [m[leaves[i]] for i in S])
+                    m[v] = D.lut(g_tt, [h] + [m[leaves[i]] for i in T])
+                else:
+                    m[v] = D.lut(C.tts[v], [m[f] for f in C.fanins[v]])
+            for group, lits in C.outputs:
+                D.output(group, [m[l >> 1] ^ (l & 1) for l in lits])
+            D = sweep(D)
+            if D.n_nodes() < C.n_nodes():
+                C, applied = D, True
+                break
+        if not applied:
+            return C
+    return C
+
+
 def optimize(C: Circuit, max_iter=8, verbose=False):
     C = sweep(C)
     best = None
     for it in range(max_iter):
         C = functional_reduce(C)
         C = lut_map(C)
+        C = resynthesize(C)
         n = C.n_nodes()
         if verbose:
             print(f"  iter {it}: {n} LUTs")
-        if best is not None and n >= best:
+        if best is not None and n >= best.n_nodes():
             break
-        best = n
-    return C
+        best = C
+    return best
