@@ -46,8 +46,9 @@ IN_FMT, ACC_FMT, OUT_FMT = (5, 3), (5, 4), (5, 4)
 # HBM bytes per launch of the convolution kernel from rocprofv3 --pmc
 # FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each scaled by what the same
 # counter reads for a plain 256 MiB device copy (FETCH x2.0, WRITE x1.0); see
-# the profiles/ summaries. None once the kernel has changed since.
-TRAFFIC = None
+# the profiles/ summaries. Set to None whenever the kernel changes, until the
+# counters are taken again.
+TRAFFIC = (3451 * 2.0 + 3136 * 1.0) * 1024   # 10.28 MB (split kernel, (5,3) -> (5,4))
 
 
 def log(*a):
@@ -110,6 +111,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=40)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup-ms", type=float, default=400.0,
+                    help="after the W warmup steps, keep running untimed steps until this "
+                         "much time has passed, so that the GPU clock has ramped up")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
@@ -167,6 +171,11 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    t_w = time.perf_counter()
+    while (time.perf_counter() - t_w) * 1e3 < args.warmup_ms:
+        for _ in range(10):
+            step()
+        torch.cuda.synchronize()
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
