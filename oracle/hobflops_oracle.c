@@ -115,6 +115,7 @@ typedef struct {
 } fields_t;
 
 static int fmt_ok(fmt_t f) { return f.wE >= 2 && f.wE <= 8 && f.wF >= 1 && f.wF <= 23; }
+static int mode_ok(int mode) { return mode == HFO_RNE || mode == HFO_RTZ; }
 static int64_t bias_of(fmt_t f) { return ((int64_t)1 << (f.wE - 1)) - 1; }
 
 static fields_t decode(uint64_t code, fmt_t f)
@@ -154,11 +155,12 @@ static int64_t exp2_of(fields_t v, fmt_t f) { return v.E - bias_of(f) - f.wF; }
 
 /* ------------------------------------------------------------------------ */
 /* Rounding: the correctly rounded code, in format f, of (-1)^s * M * 2^e
- * for an exact integer M > 0 (round to nearest, ties to even). The rounding is
- * done with an unbounded exponent; the exponent range is checked afterwards:
- * above the largest binade gives infinity, below the smallest gives zero
+ * for an exact integer M > 0, to nearest with ties to even (HFO_RNE) or toward
+ * zero (HFO_RTZ: the dropped bits are discarded). The rounding is done with an
+ * unbounded exponent; the exponent range is checked afterwards: above the
+ * largest binade gives infinity (in both modes), below the smallest gives zero
  * (there are no subnormal numbers). */
-static uint64_t round_value(fmt_t f, int s, const big* M, int64_t e)
+static uint64_t round_value(fmt_t f, int s, const big* M, int64_t e, int mode)
 {
   int p = big_bitlen(M) - 1; /* M lies in [2^p, 2^(p+1)) */
   int64_t u = p + e;         /* value lies in [2^u, 2^(u+1)) */
@@ -170,7 +172,7 @@ static uint64_t round_value(fmt_t f, int s, const big* M, int64_t e)
     sig = big_field(M, k, f.wF + 1);
     int half_bit = big_bit(M, k - 1);        /* first dropped bit */
     int below_half = big_any_below(M, k - 1); /* any later dropped bit */
-    int round_up = half_bit && (below_half || (sig & 1));
+    int round_up = mode == HFO_RNE && half_bit && (below_half || (sig & 1));
     if (round_up) sig += 1;
     if (sig == ((uint64_t)1 << (f.wF + 1))) { /* carried into a new binade */
       sig >>= 1;
@@ -186,10 +188,10 @@ static uint64_t round_value(fmt_t f, int s, const big* M, int64_t e)
 /* ------------------------------------------------------------------------ */
 /* Operations. */
 
-uint64_t hfo_mul(uint64_t a, uint64_t b, int wE, int wF_in, int wF_out)
+uint64_t hfo_mul_rm(uint64_t a, uint64_t b, int wE, int wF_in, int wF_out, int mode)
 {
   fmt_t fi = {wE, wF_in}, fo = {wE, wF_out};
-  if (!fmt_ok(fi) || !fmt_ok(fo)) return HFO_BAD_FORMAT;
+  if (!fmt_ok(fi) || !fmt_ok(fo) || !mode_ok(mode)) return HFO_BAD_FORMAT;
   fields_t A = decode(a, fi), B = decode(b, fi);
   int s = A.s ^ B.s;
   if (A.exn == EXN_NAN || B.exn == EXN_NAN) return make_nan(fo);
@@ -199,13 +201,13 @@ uint64_t hfo_mul(uint64_t a, uint64_t b, int wE, int wF_in, int wF_out)
   if (A.exn == EXN_ZERO || B.exn == EXN_ZERO) return make_zero(s, fo);
   big P;
   big_set_shl(&P, sig_of(A, fi) * sig_of(B, fi), 0); /* exact: at most 48 bits */
-  return round_value(fo, s, &P, exp2_of(A, fi) + exp2_of(B, fi));
+  return round_value(fo, s, &P, exp2_of(A, fi) + exp2_of(B, fi), mode);
 }
 
-uint64_t hfo_add(uint64_t a, uint64_t b, int wE, int wF)
+uint64_t hfo_add_rm(uint64_t a, uint64_t b, int wE, int wF, int mode)
 {
   fmt_t f = {wE, wF};
-  if (!fmt_ok(f)) return HFO_BAD_FORMAT;
+  if (!fmt_ok(f) || !mode_ok(mode)) return HFO_BAD_FORMAT;
   fields_t A = decode(a, f), B = decode(b, f);
   if (A.exn == EXN_NAN || B.exn == EXN_NAN) return make_nan(f);
   if (A.exn == EXN_INF && B.exn == EXN_INF) return A.s == B.s ? make_inf(A.s, f) : make_nan(f);
@@ -226,7 +228,7 @@ uint64_t hfo_add(uint64_t a, uint64_t b, int wE, int wF)
     s = A.s;
   } else {
     int c = big_cmp(&X, &Y);
-    if (c == 0) return make_zero(0, f); /* exact cancellation gives +0 */
+    if (c == 0) return make_zero(0, f); /* exact cancellation gives +0, in both modes */
     if (c > 0) {
       big_sub(&S, &X, &Y);
       s = A.s;
@@ -235,20 +237,32 @@ uint64_t hfo_add(uint64_t a, uint64_t b, int wE, int wF)
       s = B.s;
     }
   }
-  return round_value(f, s, &S, emin);
+  return round_value(f, s, &S, emin, mode);
 }
 
-uint64_t hfo_convert(uint64_t a, int wE, int wF_src, int wF_dst)
+uint64_t hfo_convert_rm(uint64_t a, int wE, int wF_src, int wF_dst, int mode)
 {
   fmt_t fs = {wE, wF_src}, fd = {wE, wF_dst};
-  if (!fmt_ok(fs) || !fmt_ok(fd)) return HFO_BAD_FORMAT;
+  if (!fmt_ok(fs) || !fmt_ok(fd) || !mode_ok(mode)) return HFO_BAD_FORMAT;
   fields_t A = decode(a, fs);
   if (A.exn == EXN_NAN) return make_nan(fd);
   if (A.exn == EXN_INF) return make_inf(A.s, fd);
   if (A.exn == EXN_ZERO) return make_zero(A.s, fd);
   big M;
   big_set_shl(&M, sig_of(A, fs), 0);
-  return round_value(fd, A.s, &M, exp2_of(A, fs));
+  return round_value(fd, A.s, &M, exp2_of(A, fs), mode);
+}
+
+uint64_t hfo_mul(uint64_t a, uint64_t b, int wE, int wF_in, int wF_out)
+{
+  return hfo_mul_rm(a, b, wE, wF_in, wF_out, HFO_RNE);
+}
+
+uint64_t hfo_add(uint64_t a, uint64_t b, int wE, int wF) { return hfo_add_rm(a, b, wE, wF, HFO_RNE); }
+
+uint64_t hfo_convert(uint64_t a, int wE, int wF_src, int wF_dst)
+{
+  return hfo_convert_rm(a, wE, wF_src, wF_dst, HFO_RNE);
 }
 
 uint64_t hfo_relu(uint64_t a, int wE, int wF)
@@ -261,12 +275,17 @@ uint64_t hfo_relu(uint64_t a, int wE, int wF)
   return canonical(A, f);
 }
 
+uint64_t hfo_muladd_rm(uint64_t a, uint64_t b, uint64_t c, int wE, int wF_in, int wF_acc, int mode)
+{
+  uint64_t p = hfo_mul_rm(a, b, wE, wF_in, wF_acc, mode);
+  uint64_t cw = hfo_convert_rm(c, wE, wF_in, wF_acc, mode); /* widening: exact */
+  if (p == HFO_BAD_FORMAT || cw == HFO_BAD_FORMAT) return HFO_BAD_FORMAT;
+  return hfo_add_rm(cw, p, wE, wF_acc, mode);
+}
+
 uint64_t hfo_muladd(uint64_t a, uint64_t b, uint64_t c, int wE, int wF_in, int wF_acc)
 {
-  uint64_t p = hfo_mul(a, b, wE, wF_in, wF_acc);
-  uint64_t cw = hfo_convert(c, wE, wF_in, wF_acc);
-  if (p == HFO_BAD_FORMAT || cw == HFO_BAD_FORMAT) return HFO_BAD_FORMAT;
-  return hfo_add(cw, p, wE, wF_acc);
+  return hfo_muladd_rm(a, b, c, wE, wF_in, wF_acc, HFO_RNE);
 }
 
 /* float32 -> code: the exact float32 value (subnormals included) rounded once. */
@@ -284,7 +303,7 @@ uint64_t hfo_quantize_f32(float x, int wE, int wF)
   int64_t e = ef ? (int64_t)ef - 150 : -149;
   big Mb;
   big_set_shl(&Mb, M, 0);
-  return round_value(f, s, &Mb, e);
+  return round_value(f, s, &Mb, e, HFO_RNE);
 }
 
 /* code -> float32: exact value formed in double (exact for wF <= 23 and the
@@ -369,6 +388,45 @@ int hfo_muladd_array(const uint64_t* a, const uint64_t* b, const uint64_t* c, si
   return 0;
 }
 
+int hfo_mul_rm_array(const uint64_t* a, const uint64_t* b, size_t n, int wE, int wF_in,
+                     int wF_out, int mode, uint64_t* r)
+{
+  FMT_CHECK(wE, wF_in);
+  FMT_CHECK(wE, wF_out);
+  if (!mode_ok(mode)) return -1;
+  for (size_t i = 0; i < n; i++) r[i] = hfo_mul_rm(a[i], b[i], wE, wF_in, wF_out, mode);
+  return 0;
+}
+
+int hfo_add_rm_array(const uint64_t* a, const uint64_t* b, size_t n, int wE, int wF, int mode,
+                     uint64_t* r)
+{
+  FMT_CHECK(wE, wF);
+  if (!mode_ok(mode)) return -1;
+  for (size_t i = 0; i < n; i++) r[i] = hfo_add_rm(a[i], b[i], wE, wF, mode);
+  return 0;
+}
+
+int hfo_convert_rm_array(const uint64_t* a, size_t n, int wE, int wF_src, int wF_dst, int mode,
+                         uint64_t* r)
+{
+  FMT_CHECK(wE, wF_src);
+  FMT_CHECK(wE, wF_dst);
+  if (!mode_ok(mode)) return -1;
+  for (size_t i = 0; i < n; i++) r[i] = hfo_convert_rm(a[i], wE, wF_src, wF_dst, mode);
+  return 0;
+}
+
+int hfo_muladd_rm_array(const uint64_t* a, const uint64_t* b, const uint64_t* c, size_t n, int wE,
+                        int wF_in, int wF_acc, int mode, uint64_t* r)
+{
+  FMT_CHECK(wE, wF_in);
+  FMT_CHECK(wE, wF_acc);
+  if (!mode_ok(mode)) return -1;
+  for (size_t i = 0; i < n; i++) r[i] = hfo_muladd_rm(a[i], b[i], c[i], wE, wF_in, wF_acc, mode);
+  return 0;
+}
+
 /* ------------------------------------------------------------------------ */
 /* Convolution. */
 
@@ -380,6 +438,7 @@ static int conv_ok(const hfo_conv_desc* d)
   if (d->stride < 1 || d->pad < 0) return 0;
   if (d->H + 2 * d->pad < d->KH || d->W + 2 * d->pad < d->KW) return 0;
   if (d->act != 0 && d->act != 1) return 0;
+  if (!mode_ok(d->round)) return 0;
   fmt_t a = {d->wE, d->wF_in}, b = {d->wE, d->wF_acc}, c = {d->wE, d->wF_out};
   return fmt_ok(a) && fmt_ok(b) && fmt_ok(c);
 }
@@ -403,11 +462,11 @@ static uint64_t conv_one(const uint64_t* ifm, const uint64_t* w, const hfo_conv_
         if (iy >= 0 && iy < d->H && ix >= 0 && ix < d->W)
           x = ifm[(((size_t)n * d->H + iy) * d->W + ix) * d->C + c];
         uint64_t wv = w[(((size_t)ky * d->KW + kx) * d->C + c) * d->M + m];
-        uint64_t p = hfo_mul(wv, x, d->wE, d->wF_in, d->wF_acc);
-        acc = hfo_add(acc, p, d->wE, d->wF_acc);
+        uint64_t p = hfo_mul_rm(wv, x, d->wE, d->wF_in, d->wF_acc, d->round);
+        acc = hfo_add_rm(acc, p, d->wE, d->wF_acc, d->round);
       }
   if (d->act == 1) acc = hfo_relu(acc, d->wE, d->wF_acc);
-  return hfo_convert(acc, d->wE, d->wF_acc, d->wF_out);
+  return hfo_convert_rm(acc, d->wE, d->wF_acc, d->wF_out, d->round);
 }
 
 typedef struct {

@@ -42,6 +42,15 @@ extern "C" {
 
 #define HFO_BAD_FORMAT (~(uint64_t)0)
 
+/* Rounding modes. Round to nearest, ties to even, is the paper's mode for
+ * every operation (Sec. 4); round toward zero is its second one, used for the
+ * MACs of the type sweep (Sec. 4): the dropped bits of the exact value are
+ * discarded. In both modes the exponent range is checked after rounding
+ * (overflow gives infinity) and exact cancellation gives +0. Conversion from
+ * float32 always rounds to nearest. */
+#define HFO_RNE 0
+#define HFO_RTZ 1
+
 /* Scalar operations on codes. */
 uint64_t hfo_quantize_f32(float f, int wE, int wF);
 float    hfo_decode_f32(uint64_t code, int wE, int wF);
@@ -50,6 +59,12 @@ uint64_t hfo_add(uint64_t a, uint64_t b, int wE, int wF);
 uint64_t hfo_convert(uint64_t a, int wE, int wF_src, int wF_dst);
 uint64_t hfo_relu(uint64_t a, int wE, int wF);
 uint64_t hfo_muladd(uint64_t a, uint64_t b, uint64_t c, int wE, int wF_in, int wF_acc);
+/* The same with an explicit rounding mode (HFO_RNE or HFO_RTZ; any other
+ * value gives HFO_BAD_FORMAT). */
+uint64_t hfo_mul_rm(uint64_t a, uint64_t b, int wE, int wF_in, int wF_out, int mode);
+uint64_t hfo_add_rm(uint64_t a, uint64_t b, int wE, int wF, int mode);
+uint64_t hfo_convert_rm(uint64_t a, int wE, int wF_src, int wF_dst, int mode);
+uint64_t hfo_muladd_rm(uint64_t a, uint64_t b, uint64_t c, int wE, int wF_in, int wF_acc, int mode);
 
 /* Element-wise array forms (same semantics, n elements). Return 0, or -1 on a
  * bad format. */
@@ -62,6 +77,14 @@ int hfo_convert_array(const uint64_t* a, size_t n, int wE, int wF_src, int wF_ds
 int hfo_relu_array(const uint64_t* a, size_t n, int wE, int wF, uint64_t* r);
 int hfo_muladd_array(const uint64_t* a, const uint64_t* b, const uint64_t* c, size_t n, int wE,
                      int wF_in, int wF_acc, uint64_t* r);
+int hfo_mul_rm_array(const uint64_t* a, const uint64_t* b, size_t n, int wE, int wF_in,
+                     int wF_out, int mode, uint64_t* r);
+int hfo_add_rm_array(const uint64_t* a, const uint64_t* b, size_t n, int wE, int wF, int mode,
+                     uint64_t* r);
+int hfo_convert_rm_array(const uint64_t* a, size_t n, int wE, int wF_src, int wF_dst, int mode,
+                         uint64_t* r);
+int hfo_muladd_rm_array(const uint64_t* a, const uint64_t* b, const uint64_t* c, size_t n, int wE,
+                        int wF_in, int wF_acc, int mode, uint64_t* r);
 
 /* Multi-channel multi-kernel convolution (paper, Sec. 3.4).
  * ifm: codes in in_fmt, NHWC [N][H][W][C]; w: codes in in_fmt, HWIO
@@ -70,11 +93,14 @@ int hfo_muladd_array(const uint64_t* a, const uint64_t* b, const uint64_t* c, si
  * For every output: acc = +0 in acc_fmt; for ky, then kx, then c:
  *   acc = add(acc, mul(w[ky][kx][c][m], x)), x = +0 for a padding tap;
  * then ofm = convert(act(acc), acc_fmt -> out_fmt); act 0 = none, 1 = ReLU.
+ * Every mul, add and the final convert round in mode `round` (HFO_RNE or
+ * HFO_RTZ).
  * All formats share wE. nthreads <= 0 means one thread per online CPU.
  * Returns 0, or -1 on bad arguments. */
 typedef struct {
   int N, H, W, C, M, KH, KW, stride, pad;
   int wE, wF_in, wF_acc, wF_out, act;
+  int round;
 } hfo_conv_desc;
 
 int hfo_conv2d(const uint64_t* ifm, const uint64_t* w, uint64_t* ofm, const hfo_conv_desc* d,

@@ -16,7 +16,9 @@ _lib = None
 class ConvDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int) for n in
                 ("N", "H", "W", "C", "M", "KH", "KW", "stride", "pad",
-                 "wE", "wF_in", "wF_acc", "wF_out", "act")]
+                 "wE", "wF_in", "wF_acc", "wF_out", "act", "round")]
+
+RNE, RTZ = 0, 1  # rounding modes: nearest with ties to even, toward zero
 
 
 def load(path):
@@ -33,11 +35,17 @@ def load(path):
     L.hfo_convert_array.argtypes = [u64p, sz, ci, ci, ci, u64p]
     L.hfo_relu_array.argtypes = [u64p, sz, ci, ci, u64p]
     L.hfo_muladd_array.argtypes = [u64p, u64p, u64p, sz, ci, ci, ci, u64p]
+    L.hfo_mul_rm_array.argtypes = [u64p, u64p, sz, ci, ci, ci, ci, u64p]
+    L.hfo_add_rm_array.argtypes = [u64p, u64p, sz, ci, ci, ci, u64p]
+    L.hfo_convert_rm_array.argtypes = [u64p, sz, ci, ci, ci, ci, u64p]
+    L.hfo_muladd_rm_array.argtypes = [u64p, u64p, u64p, sz, ci, ci, ci, ci, u64p]
     L.hfo_conv2d.argtypes = [u64p, u64p, u64p, ctypes.POINTER(ConvDesc), ci]
     L.hfo_conv2d_points.argtypes = [u64p, u64p, i64p, sz, u64p, ctypes.POINTER(ConvDesc), ci]
     for name in ("hfo_quantize_f32_array", "hfo_decode_f32_array", "hfo_mul_array",
                  "hfo_add_array", "hfo_convert_array", "hfo_relu_array",
                  "hfo_muladd_array", "hfo_conv2d", "hfo_conv2d_points",
+                 "hfo_mul_rm_array", "hfo_add_rm_array", "hfo_convert_rm_array",
+                 "hfo_muladd_rm_array",
                  "hfo_default_threads"):
         getattr(L, name).restype = ctypes.c_int
     return L
@@ -82,29 +90,29 @@ def decode_f32(codes, wE, wF, L=None):
     return r
 
 
-def mul(a, b, wE, wF_in, wF_out, L=None):
+def mul(a, b, wE, wF_in, wF_out, L=None, rnd=RNE):
     a, b = np.broadcast_arrays(_u64(a), _u64(b))
     a, b = _u64(a), _u64(b)
     r = np.empty(a.shape, np.uint64)
-    _check((L or lib()).hfo_mul_array(_p(a, ctypes.c_uint64), _p(b, ctypes.c_uint64), a.size, wE, wF_in,
-                               wF_out, _p(r, ctypes.c_uint64)))
+    _check((L or lib()).hfo_mul_rm_array(_p(a, ctypes.c_uint64), _p(b, ctypes.c_uint64), a.size, wE,
+                                         wF_in, wF_out, rnd, _p(r, ctypes.c_uint64)))
     return r
 
 
-def add(a, b, wE, wF, L=None):
+def add(a, b, wE, wF, L=None, rnd=RNE):
     a, b = np.broadcast_arrays(_u64(a), _u64(b))
     a, b = _u64(a), _u64(b)
     r = np.empty(a.shape, np.uint64)
-    _check((L or lib()).hfo_add_array(_p(a, ctypes.c_uint64), _p(b, ctypes.c_uint64), a.size, wE, wF,
-                               _p(r, ctypes.c_uint64)))
+    _check((L or lib()).hfo_add_rm_array(_p(a, ctypes.c_uint64), _p(b, ctypes.c_uint64), a.size, wE,
+                                         wF, rnd, _p(r, ctypes.c_uint64)))
     return r
 
 
-def convert(a, wE, wF_src, wF_dst, L=None):
+def convert(a, wE, wF_src, wF_dst, L=None, rnd=RNE):
     a = _u64(a)
     r = np.empty(a.shape, np.uint64)
-    _check((L or lib()).hfo_convert_array(_p(a, ctypes.c_uint64), a.size, wE, wF_src, wF_dst,
-                                   _p(r, ctypes.c_uint64)))
+    _check((L or lib()).hfo_convert_rm_array(_p(a, ctypes.c_uint64), a.size, wE, wF_src, wF_dst,
+                                             rnd, _p(r, ctypes.c_uint64)))
     return r
 
 
@@ -115,28 +123,29 @@ def relu(a, wE, wF, L=None):
     return r
 
 
-def muladd(a, b, c, wE, wF_in, wF_acc, L=None):
+def muladd(a, b, c, wE, wF_in, wF_acc, L=None, rnd=RNE):
     a, b, c = np.broadcast_arrays(_u64(a), _u64(b), _u64(c))
     a, b, c = _u64(a), _u64(b), _u64(c)
     r = np.empty(a.shape, np.uint64)
-    _check((L or lib()).hfo_muladd_array(_p(a, ctypes.c_uint64), _p(b, ctypes.c_uint64),
-                                  _p(c, ctypes.c_uint64), a.size, wE, wF_in, wF_acc,
-                                  _p(r, ctypes.c_uint64)))
+    _check((L or lib()).hfo_muladd_rm_array(_p(a, ctypes.c_uint64), _p(b, ctypes.c_uint64),
+                                            _p(c, ctypes.c_uint64), a.size, wE, wF_in, wF_acc,
+                                            rnd, _p(r, ctypes.c_uint64)))
     return r
 
 
-def _desc(ifm_shape, w_shape, stride, pad, wE, wF_in, wF_acc, wF_out, act):
+def _desc(ifm_shape, w_shape, stride, pad, wE, wF_in, wF_acc, wF_out, act, rnd):
     N, H, W, C = ifm_shape
     KH, KW, C2, M = w_shape
     if C2 != C:
         raise ValueError("channel mismatch between IFM and weights")
-    return ConvDesc(N, H, W, C, M, KH, KW, stride, pad, wE, wF_in, wF_acc, wF_out, int(act))
+    return ConvDesc(N, H, W, C, M, KH, KW, stride, pad, wE, wF_in, wF_acc, wF_out, int(act),
+                    int(rnd))
 
 
-def conv2d(ifm, w, stride, pad, wE, wF_in, wF_acc, wF_out, act=0, nthreads=0, L=None):
+def conv2d(ifm, w, stride, pad, wE, wF_in, wF_acc, wF_out, act=0, nthreads=0, L=None, rnd=RNE):
     """Full convolution: ifm [N,H,W,C] and w [KH,KW,C,M] codes -> [N,OH,OW,M] codes."""
     ifm, w = _u64(ifm), _u64(w)
-    d = _desc(ifm.shape, w.shape, stride, pad, wE, wF_in, wF_acc, wF_out, act)
+    d = _desc(ifm.shape, w.shape, stride, pad, wE, wF_in, wF_acc, wF_out, act, rnd)
     OH = (d.H + 2 * pad - d.KH) // stride + 1
     OW = (d.W + 2 * pad - d.KW) // stride + 1
     r = np.empty((d.N, OH, OW, d.M), np.uint64)
@@ -146,11 +155,11 @@ def conv2d(ifm, w, stride, pad, wE, wF_in, wF_acc, wF_out, act=0, nthreads=0, L=
 
 
 def conv2d_points(ifm, w, pts, stride, pad, wE, wF_in, wF_acc, wF_out, act=0, nthreads=0,
-                  L=None):
+                  L=None, rnd=RNE):
     """Convolution outputs at the (n, oy, ox, m) rows of pts only."""
     ifm, w = _u64(ifm), _u64(w)
     pts = np.ascontiguousarray(pts, dtype=np.int64).reshape(-1, 4)
-    d = _desc(ifm.shape, w.shape, stride, pad, wE, wF_in, wF_acc, wF_out, act)
+    d = _desc(ifm.shape, w.shape, stride, pad, wE, wF_in, wF_acc, wF_out, act, rnd)
     r = np.empty(len(pts), np.uint64)
     _check((L or lib()).hfo_conv2d_points(_p(ifm, ctypes.c_uint64), _p(w, ctypes.c_uint64),
                                    _p(pts, ctypes.c_int64), len(pts), _p(r, ctypes.c_uint64),

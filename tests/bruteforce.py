@@ -4,7 +4,8 @@ It shares no code or structure with the oracle's rounding: values are formed
 with IEEE float64 arithmetic (exact for the small formats used here, and IEEE
 semantics decide NaN, infinity and zero signs), and rounding is a search for
 the nearest element of the sorted list of representable values, ties going to
-the element whose fraction field is even. The list spans an unbounded exponent
+the element whose fraction field is even (or, toward zero, for the element of
+largest magnitude not above the value's). The list spans an unbounded exponent
 range around the data, so "round first, then check the exponent range" falls
 out of the search.
 
@@ -41,9 +42,10 @@ def _grid(wF, umin, umax):
     return vals, u, f
 
 
-def nearest(v, wE, wF):
+def nearest(v, wE, wF, mode="rne"):
     """Codes of float64 values v (any mix of finite, infinite, NaN, signed zero),
-    rounded to nearest with ties to even fraction, then range checked."""
+    rounded to nearest with ties to even fraction (mode "rne") or toward zero
+    ("rtz"), then range checked."""
     v = np.asarray(v, dtype=np.float64)
     bias = (1 << (wE - 1)) - 1
     out = np.zeros(v.shape, np.uint64)
@@ -67,7 +69,10 @@ def nearest(v, wE, wF):
         lo = vals[i - 1]
         d_hi = hi - a  # exact: lo and hi are within a factor two of a
         d_lo = a - lo
-        pick_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (gf[i] % 2 == 0))
+        if mode == "rtz":
+            pick_hi = d_hi == 0
+        else:
+            pick_hi = (d_hi < d_lo) | ((d_hi == d_lo) & (gf[i] % 2 == 0))
         j = np.where(pick_hi, i, i - 1)
         u, f = gu[j], gf[j]
         Eb = u + bias
@@ -80,16 +85,17 @@ def nearest(v, wE, wF):
     return out
 
 
-def mul(a, b, wE, wF_in, wF_out):
-    return nearest(to_float64(a, wE, wF_in) * to_float64(b, wE, wF_in), wE, wF_out)
+def mul(a, b, wE, wF_in, wF_out, mode="rne"):
+    return nearest(to_float64(a, wE, wF_in) * to_float64(b, wE, wF_in), wE, wF_out, mode)
 
 
-def add(a, b, wE, wF):
-    return nearest(to_float64(a, wE, wF) + to_float64(b, wE, wF), wE, wF)
+def add(a, b, wE, wF, mode="rne"):
+    # IEEE float64 gives +0 for x + (-x), which is this format's rule in both modes
+    return nearest(to_float64(a, wE, wF) + to_float64(b, wE, wF), wE, wF, mode)
 
 
-def convert(a, wE, wF_src, wF_dst):
-    return nearest(to_float64(a, wE, wF_src), wE, wF_dst)
+def convert(a, wE, wF_src, wF_dst, mode="rne"):
+    return nearest(to_float64(a, wE, wF_src), wE, wF_dst, mode)
 
 
 def relu(a, wE, wF):

@@ -9,7 +9,7 @@ from paper_2007_06563_amd import inputs as I
 WE, WF, WACC = 5, 3, 4
 
 
-def ref_conv(ifm, w, stride, pad, wE, wF_in, wF_acc, wF_out, act=0):
+def ref_conv(ifm, w, stride, pad, wE, wF_in, wF_acc, wF_out, act=0, mode="rne"):
     """Convolution written as the plain loop over (ky, kx, c) with the
     brute-force reference operations, vectorised over all outputs at once."""
     N, H, W, C = ifm.shape
@@ -26,10 +26,10 @@ def ref_conv(ifm, w, stride, pad, wE, wF_in, wF_acc, wF_out, act=0):
                 x = padded[:, ky:ky + stride * OH:stride, kx:kx + stride * OW:stride, c]
                 x = np.broadcast_to(x[..., None], acc.shape)
                 wv = np.broadcast_to(w[ky, kx, c, :], acc.shape)
-                acc = bf.add(acc, bf.mul(wv, x, wE, wF_in, wF_acc), wE, wF_acc)
+                acc = bf.add(acc, bf.mul(wv, x, wE, wF_in, wF_acc, mode), wE, wF_acc, mode)
     if act:
         acc = bf.relu(acc, wE, wF_acc)
-    return bf.convert(acc, wE, wF_acc, wF_out)
+    return bf.convert(acc, wE, wF_acc, wF_out, mode)
 
 
 def small_conv_codes():

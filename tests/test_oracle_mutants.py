@@ -18,8 +18,16 @@ from test_oracle_conv import ref_conv
 SRC = open(obuild.SRC).read()
 
 MUTANTS = {
-    "ties_away": ("int round_up = half_bit && (below_half || (sig & 1));", "int round_up = half_bit;"),
-    "truncate": ("int round_up = half_bit && (below_half || (sig & 1));", "int round_up = 0;"),
+    "ties_away": ("int round_up = mode == HFO_RNE && half_bit && (below_half || (sig & 1));",
+                  "int round_up = mode == HFO_RNE && half_bit;"),
+    "truncate": ("int round_up = mode == HFO_RNE && half_bit && (below_half || (sig & 1));",
+                 "int round_up = 0;"),
+    "rtz_rounds_to_nearest": ("int round_up = mode == HFO_RNE && half_bit && (below_half || (sig & 1));",
+                              "int round_up = half_bit && (below_half || (sig & 1));"),
+    "rtz_rounds_up": ("int round_up = mode == HFO_RNE && half_bit && (below_half || (sig & 1));",
+                      "int round_up = mode == HFO_RNE ? half_bit && (below_half || (sig & 1)) : (half_bit || below_half);"),
+    "conv_ignores_mode": ("acc = hfo_add_rm(acc, p, d->wE, d->wF_acc, d->round);",
+                          "acc = hfo_add_rm(acc, p, d->wE, d->wF_acc, HFO_RNE);"),
     "sticky_dropped": ("int below_half = big_any_below(M, k - 1);", "int below_half = 0;"),
     "no_renormalise": ("sig >>= 1;\n      u += 1;", "sig >>= 1;"),
     "bias_off_by_one": ("return ((int64_t)1 << (f.wE - 1)) - 1;", "return ((int64_t)1 << (f.wE - 1));"),
@@ -32,7 +40,8 @@ MUTANTS = {
                        "if (0)"),
     "inf_minus_inf": ("return A.s == B.s ? make_inf(A.s, f) : make_nan(f);", "return make_inf(A.s, f);"),
     "sub_sign": ("      s = B.s;", "      s = A.s;"),
-    "product_exponent": ("exp2_of(A, fi) + exp2_of(B, fi));", "exp2_of(A, fi) + exp2_of(B, fi) + 1);"),
+    "product_exponent": ("exp2_of(A, fi) + exp2_of(B, fi), mode);",
+                         "exp2_of(A, fi) + exp2_of(B, fi) + 1, mode);"),
     "align_wrong_operand": ("big_set_shl(&Y, sig_of(B, f), (int)(eb - emin));",
                             "big_set_shl(&Y, sig_of(B, f), (int)(ea - emin));"),
     "relu_keeps_neg_zero": ("if (A.s) return make_zero(0, f);",
@@ -42,8 +51,8 @@ MUTANTS = {
     "subnormal_scale": ("int64_t e = ef ? (int64_t)ef - 150 : -149;", "int64_t e = ef ? (int64_t)ef - 150 : -150;"),
     "channel_order": ("for (int c = 0; c < d->C; c++) {", "for (int c = d->C - 1; c >= 0; c--) {"),
     "padding_index": ("int ix = ox * d->stride + kx - d->pad;", "int ix = ox * d->stride + kx;"),
-    "relu_after_convert": ("  if (d->act == 1) acc = hfo_relu(acc, d->wE, d->wF_acc);\n  return hfo_convert(acc, d->wE, d->wF_acc, d->wF_out);",
-                           "  return hfo_convert(acc, d->wE, d->wF_acc, d->wF_out);"),
+    "relu_after_convert": ("  if (d->act == 1) acc = hfo_relu(acc, d->wE, d->wF_acc);\n  return hfo_convert_rm(",
+                           "  return hfo_convert_rm("),
 }
 
 
@@ -76,6 +85,9 @@ def refs():
     ifm = bf.quantize(g.uniform(-2, 2, (1, 5, 6, 4)).astype(np.float32), 5, 3)
     w = bf.quantize(g.uniform(-1, 1, (3, 3, 4, 3)).astype(np.float32), 5, 3)
     r["conv"] = (ifm, w, ref_conv(ifm, w, 1, 1, 5, 3, 4, 4), ref_conv(ifm, w, 1, 1, 5, 3, 4, 4, act=1))
+    r["mul_rtz"] = bf.mul(a, b, 5, 3, 4, mode="rtz")
+    r["add_rtz"] = bf.add(a2, b2, 4, 3, mode="rtz")
+    r["conv_rtz"] = ref_conv(ifm, w, 1, 1, 5, 3, 4, 3, mode="rtz")
     return r
 
 
@@ -100,6 +112,14 @@ def failures(L, r):
         bad.append("conv")
     if not np.array_equal(orc.conv2d(ifm, w, 1, 1, 5, 3, 4, 4, act=1, L=L), want_relu):
         bad.append("conv_relu")
+    a, b, _ = r["mul"]
+    if not np.array_equal(orc.mul(a, b, 5, 3, 4, L=L, rnd=orc.RTZ), r["mul_rtz"]):
+        bad.append("mul_rtz")
+    a, b, _ = r["add"]
+    if not np.array_equal(orc.add(a, b, 4, 3, L=L, rnd=orc.RTZ), r["add_rtz"]):
+        bad.append("add_rtz")
+    if not np.array_equal(orc.conv2d(ifm, w, 1, 1, 5, 3, 4, 3, L=L, rnd=orc.RTZ), r["conv_rtz"]):
+        bad.append("conv_rtz")
     return bad
 
 
