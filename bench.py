@@ -106,6 +106,115 @@ def cpu_baseline(ifm, w, s, gpu_codes, seconds):
     }
 
 
+def _time(fn, reps, stream):
+    """Average ms of fn() over reps launches (HIP events on the stream)."""
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def _conv_ops(d):
+    """(algorithm the library picks, VALU ops per 32-MAC word of that kernel)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    P = d.N * hf.conv_out_hw(d)[0] * hf.conv_out_hw(d)[1]
+    chain_waves = ((P + 63) // 64) * ((d.M + 31) // 32)
+    algo = hf.ALGO_SPLIT if chain_waves <= 4 * cus else hf.ALGO_FUSED
+    ops = hf.netlist_ops((d.in_fmt.wE, d.in_fmt.wF), (d.acc_fmt.wE, d.acc_fmt.wF))
+    return algo, (ops["mul"] + ops["accum"] if algo == hf.ALGO_SPLIT else ops["mac"])
+
+
+def suite(reps):
+    """One JSON line per further workload: the element-wise sweep and
+    pack/unpack against HBM, the mantissa sweep and the 13-layer stack
+    against the VALU peak. Inputs resident in HBM; kernels only."""
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    for idx, (wE, wF) in enumerate(I.FMA_FORMATS):
+        a, b, c = (torch.from_numpy(t.reshape(1, -1)).to(dev) for t in I.fma_operands(idx))
+        n = a.numel()
+        f, fa = (wE, wF), (wE, wF + 1)
+        pa, pb, pc = (hf.pack(t, f) for t in (a, b, c))
+        r = hf.muladd(pa, pb, pc, n, f, fa)
+        ms = _time(lambda: hf.muladd(pa, pb, pc, n, f, fa, out=r), reps, stream)
+        nbytes = (3 * pa.numel() + r.numel()) * 4
+        ms_pack = _time(lambda: hf.pack(a, f, out=pa), reps, stream)
+        ms_unpack = _time(lambda: hf.unpack(r, 1, n, fa, kind="f32"), reps, stream)
+        print(json.dumps({
+            "workload": f"element-wise a*b+c, 2^24 triples, ({wE},{wF}) -> ({wE},{wF + 1})",
+            "kernel": "muladd_kernel", "ms": ms, "gops": n / (ms * 1e-3) / 1e9,
+            "roofline": {"bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9, "peak": 8000.0,
+                         "unit": "GB/s", "frac": nbytes / (ms * 1e-3) / HBM_PEAK},
+            "pack_gbps": (n * 4 + pa.numel() * 4) / (ms_pack * 1e-3) / 1e9,
+            "unpack_gbps": (r.numel() * 4 + n * 4) / (ms_unpack * 1e-3) / 1e9}), flush=True)
+        del a, b, c, pa, pb, pc, r
+    for si, s in enumerate(I.MANTISSA_SWEEP_SHAPES):
+        for m in I.MANTISSA_SWEEP_WF:
+            ifm, w = I.conv_inputs(I.MANTISSA_SWEEP, 16 * si + m, s)
+            d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, (5, m),
+                             (5, m + 1), (5, m + 1))
+            pi = hf.pack(torch.from_numpy(ifm.reshape(-1, s.C)).to(dev), (5, m))
+            pw = hf.pack(torch.from_numpy(w.reshape(-1, s.M)).to(dev), (5, m))
+            o = hf.conv2d(pi, pw, d)
+            ms = _time(lambda: hf.conv2d(pi, pw, d, out=o), reps, stream)
+            algo, G = _conv_ops(d)
+            lane_ops = s.macs / 32.0 * G
+            print(json.dumps({
+                "workload": f"conv {s.N}x{s.H}x{s.W}x{s.C} -> {s.M} 3x3, (5,{m}) -> (5,{m + 1})",
+                "kernel": "split" if algo == hf.ALGO_SPLIT else "fused", "ms": ms,
+                "gmacs": s.macs / (ms * 1e-3) / 1e9, "ops_per_mac_word": G,
+                "roofline": {"bound": "alu", "achieved": lane_ops / (ms * 1e-3) / 1e12,
+                             "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
+                             "frac": lane_ops / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
+    shapes = I.resnet_stack_shapes(16)
+    fmts = I.resnet_stack_formats(len(shapes))
+    ifm0, _ = I.conv_inputs(I.RESNET_STACK, 0, shapes[0])
+    x0 = hf.pack(torch.from_numpy(ifm0.reshape(-1, shapes[0].C)).to(dev), (5, fmts[0][0]))
+    layers = []
+    for li, (s, (wi, wa, wo)) in enumerate(zip(shapes, fmts)):
+        _, w = I.conv_inputs(I.RESNET_STACK, li, s)
+        d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, (5, wi), (5, wa),
+                         (5, wo), hf.ACT_RELU)
+        pw = hf.pack(torch.from_numpy(w.reshape(-1, s.M)).to(dev), (5, wi))
+        layers.append((s, d, pw))
+    acts = [x0]
+    for s, d, pw in layers:
+        acts.append(hf.conv2d(acts[-1], pw, d))
+    total_ms, total_macs, total_ops = 0.0, 0, 0.0
+    for li, (s, d, pw) in enumerate(layers):
+        src, dst = acts[li], acts[li + 1]
+        ms = _time(lambda: hf.conv2d(src, pw, d, out=dst), reps, stream)
+        algo, G = _conv_ops(d)
+        total_ms += ms
+        total_macs += s.macs
+        total_ops += s.macs / 32.0 * G
+        print(json.dumps({
+            "workload": f"stack layer {li + 1}: {s.N}x{s.H}x{s.W}x{s.C} -> {s.M} {s.KH}x{s.KW} "
+                        f"s{s.stride}, (5,{fmts[li][0]}) -> (5,{fmts[li][1]}) -> (5,{fmts[li][2]}) "
+                        "relu",
+            "kernel": "split" if algo == hf.ALGO_SPLIT else "fused", "ms": ms,
+            "gmacs": s.macs / (ms * 1e-3) / 1e9, "ops_per_mac_word": G,
+            "roofline": {"bound": "alu", "achieved": s.macs / 32.0 * G / (ms * 1e-3) / 1e12,
+                         "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
+                         "frac": s.macs / 32.0 * G / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
+
+    def whole():
+        for li, (s, d, pw) in enumerate(layers):
+            hf.conv2d(acts[li], pw, d, out=acts[li + 1])
+    ms = _time(whole, max(1, reps // 4), stream)
+    print(json.dumps({
+        "workload": "13-layer stack, batch 16, 56x56x64 input, planes resident between layers",
+        "ms": ms, "sum_of_layers_ms": total_ms, "gmacs": total_macs / (ms * 1e-3) / 1e9,
+        "roofline": {"bound": "alu", "achieved": total_ops / (ms * 1e-3) / 1e12,
+                     "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
+                     "frac": total_ops / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -119,6 +228,9 @@ def main():
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB "
                          "(steps times): the reference for scaling HBM byte counters")
+    ap.add_argument("--suite", action="store_true",
+                    help="instead of the one-line benchmark: one JSON line per further workload "
+                         "(element-wise sweep, mantissa sweep, 13-layer stack)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the layer shards "
@@ -127,6 +239,9 @@ def main():
         sys.exit(2)
     torch.cuda.init()
     dev = torch.device("cuda:0")
+    if args.suite:
+        suite(args.steps)
+        return
     if args.calibrate_copy_mib:
         n = args.calibrate_copy_mib * (1 << 20) // 4
         a = torch.ones(n, dtype=torch.float32, device=dev)

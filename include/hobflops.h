@@ -26,9 +26,10 @@
  *  - Arguments are checked before anything is launched; a rejected call
  *    launches nothing and returns a negative status (see below).
  *  - Supported widths: 2 <= wE <= 8, 1 <= wF <= 23, NB <= 32. The convolution
- *    and element-wise MAC run only for the format combinations the library was
- *    generated for (hobflops_conv2d_supported / hobflops_muladd_supported);
- *    other combinations return HOBFLOPS_EUNSUPPORTED.
+ *    and element-wise MAC run only for the format combinations and rounding
+ *    modes the library was generated for (hobflops_conv2d_supported /
+ *    hobflops_muladd_supported); other combinations return
+ *    HOBFLOPS_EUNSUPPORTED.
  *  - The library keeps no state between calls and is safe to call from
  *    several host threads.
  */
@@ -56,7 +57,12 @@ enum {
 };
 
 enum { HOBFLOPS_SRC_F32 = 0, HOBFLOPS_SRC_CODE_U32 = 1 };
-enum { HOBFLOPS_ROUND_NEAREST_EVEN = 0 };
+/* Rounding of the multiply-accumulate operations (paper Sec. 4): to nearest
+ * with ties to even, or toward zero (the dropped bits of the exact value are
+ * discarded). In both modes the exponent range is checked after rounding, so
+ * an overflow gives a signed infinity, and an exact cancellation gives +0.
+ * hobflops_pack always rounds to nearest even. */
+enum { HOBFLOPS_ROUND_NEAREST_EVEN = 0, HOBFLOPS_ROUND_TOWARD_ZERO = 1 };
 enum { HOBFLOPS_ORDER_KY_KX_C = 0 };
 enum { HOBFLOPS_ACT_NONE = 0, HOBFLOPS_ACT_RELU = 1 };
 /* Kernel shape of hobflops_conv2d (results are identical for all three):
@@ -97,8 +103,12 @@ int hobflops_unpack(const uint32_t* planes, int64_t rows, int64_t len, hobflops_
  *   acc = add(acc, mul(w[ky][kx][c][m], x)), x the IFM value or +0 for a
  *   padding tap, mul rounding into acc_fmt and add rounding in acc_fmt; then
  *   ofm = convert(act(acc)) into out_fmt (ReLU: NaN stays NaN, negatives and -0
- *   give +0). All formats share wE; acc_fmt.wF >= in_fmt.wF.
- *   round must be HOBFLOPS_ROUND_NEAREST_EVEN, order HOBFLOPS_ORDER_KY_KX_C. */
+ *   give +0). All formats share wE; acc_fmt.wF >= in_fmt.wF. With
+ *   acc_fmt.wF = in_fmt.wF + 1 this is the paper's "single" MAC type, with
+ *   2 * in_fmt.wF + 1 its "extended" type, whose products are exact (Table 3).
+ *   round: HOBFLOPS_ROUND_* for every mul, add and the final convert; order
+ *   must be HOBFLOPS_ORDER_KY_KX_C. algo SPLIT returns HOBFLOPS_EUNSUPPORTED
+ *   for a variant generated without the split kernel; AUTO then runs FUSED. */
 typedef struct {
   int N, H, W, C, M, KH, KW, stride, pad;
   hobflops_fmt in_fmt, acc_fmt, out_fmt;
@@ -109,26 +119,29 @@ typedef struct {
 int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
                     const hobflops_conv_desc* d, void* stream);
 
-/* 1 if hobflops_conv2d has a kernel for d's formats and activation, else 0. */
+/* 1 if hobflops_conv2d has a kernel for d's formats, activation, rounding
+ * mode and (for HOBFLOPS_ALGO_SPLIT) kernel shape, else 0. */
 int hobflops_conv2d_supported(const hobflops_conv_desc* d);
 
 /* Element-wise r = add(widen(c), mul(a, b)) over n elements of flat PL32
  * tensors (rows 1, len n): a, b, c in in_fmt, r in acc_fmt (same wE,
  * acc_fmt.wF >= in_fmt.wF); the product is rounded into acc_fmt, c widened
  * exactly, the sum rounded once more (the paper's MAC: a multiplier then an
- * adder, Sec. 3.3 and Table 3). */
+ * adder, Sec. 3.3 and Table 3), both in mode round (HOBFLOPS_ROUND_*). */
 int hobflops_muladd(const uint32_t* a, const uint32_t* b, const uint32_t* c, uint32_t* r,
-                    int64_t n, hobflops_fmt in_fmt, hobflops_fmt acc_fmt, void* stream);
+                    int64_t n, hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int round,
+                    void* stream);
 
-int hobflops_muladd_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt);
+int hobflops_muladd_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int round);
 
 /* Bitwise VALU instructions per 32-lane word in the generated netlists of a
- * MAC (in_fmt x in_fmt -> acc_fmt, then acc_fmt + acc_fmt): the convolution's
- * fused multiply-add step, its multiplier and its accumulating adder alone
- * (the split kernel's two wave roles), and the element-wise kernel's MAC (the
- * paper's gate count, Sec. 4: throughput follows it). Returns HOBFLOPS_OK or
- * HOBFLOPS_EUNSUPPORTED; any output pointer may be NULL. */
-int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int* conv_mac_ops,
+ * MAC (in_fmt x in_fmt -> acc_fmt, then acc_fmt + acc_fmt, rounding mode
+ * round): the convolution's fused multiply-add step, its multiplier and its
+ * accumulating adder alone (the split kernel's two wave roles; 0 where that
+ * kernel was not generated), and the element-wise kernel's MAC (the paper's
+ * gate count, Sec. 4: throughput follows it). Returns HOBFLOPS_OK,
+ * HOBFLOPS_EINVAL or HOBFLOPS_EUNSUPPORTED; any output pointer may be NULL. */
+int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int round, int* conv_mac_ops,
                          int* conv_mul_ops, int* conv_accum_ops, int* muladd_ops);
 
 /* Text for a status code; for HOBFLOPS_EHIP, the last HIP error of this

@@ -28,7 +28,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 from paper_2007_06563_amd import variants  # noqa: E402
-from paper_2007_06563_amd.gen import asmgen, emit, fp, opt  # noqa: E402
+from paper_2007_06563_amd.gen import asmgen, emit, fp, opt, regalloc  # noqa: E402
 
 
 def nb(wE, wF):
@@ -42,32 +42,38 @@ def _gen_sources_digest():
     return h.hexdigest()[:16]
 
 
-def netlist(kind, key, cache):
-    """Optimised circuit for one operator; cached per generator version."""
+def netlist(kind, key, rnd, cache):
+    """Optimised circuit for one operator (rounding mode rnd: variants.RNE or
+    RTZ); cached per generator version."""
     name = {"mac": "mac_e{}m{}_a{}", "epi": "epi_e{}m{}_o{}{}", "muladd": "muladd_e{}m{}_a{}",
             "prod": "prod_e{}m{}_a{}", "accum": "accum_e{}m{}"}[kind]
+    r = variants.RND_NAME[rnd]
+    sfx = variants._sfx(rnd)
     if kind == "epi":
         wE, wa, wo, act = key
-        fname = name.format(wE, wa, wo, "_relu" if act else "")
+        # a widening convert rounds nothing: one netlist serves both modes
+        if wo >= wa:
+            r, sfx = "rne", ""
+        fname = name.format(wE, wa, wo, "_relu" if act else "") + sfx
     else:
-        fname = name.format(*key)
+        fname = name.format(*key) + sfx
     if fname in cache:
         return fname, cache[fname]
     if kind == "mac":
-        C = fp.mac_circuit(*key)
+        C = fp.mac_circuit(*key, rnd=r)
         text_kw = {"in_place": "acc"}
     elif kind == "prod":
-        C = fp.product_circuit(*key)
+        C = fp.product_circuit(*key, rnd=r)
         text_kw = {}
     elif kind == "accum":
-        C = fp.accumulate_circuit(*key)
+        C = fp.accumulate_circuit(*key, rnd=r)
         text_kw = {"in_place": "acc"}
     elif kind == "epi":
         wE, wa, wo, act = key
-        C = fp.convert_circuit(wE, wa, wo, relu=bool(act), canonical=True)
+        C = fp.convert_circuit(wE, wa, wo, relu=bool(act), canonical=True, rnd=r)
         text_kw = {}
     else:
-        C = fp.muladd_circuit(*key)
+        C = fp.muladd_circuit(*key, rnd=r)
         text_kw = {}
     raw = C.n_nodes()
     C = opt.optimize(C)
@@ -83,16 +89,22 @@ def split_batch(naccp):
     return 4 if 2 * 4 * 256 * naccp * 4 <= 128 * 1024 else 2
 
 
-def split_asm(wE, wi, wa, cache):
-    key = f"split_e{wE}m{wi}_a{wa}"
+def split_asm(wE, wi, wa, rnd, cache):
+    """The split kernel's assembly for one variant, or None when the two
+    netlists do not fit the registers the asm blocks may use."""
+    key = f"split_e{wE}m{wi}_a{wa}{variants._sfx(rnd)}"
     if key not in cache:
+        r = variants.RND_NAME[rnd]
         nin, nacc = nb(wE, wi), nb(wE, wa)
-        acc_c = opt.optimize(fp.accumulate_circuit(wE, wa))
-        prod_c = opt.optimize(fp.product_circuit(wE, wi, wa))
-        text, stats = asmgen.split_functions(acc_c, prod_c, nin, nacc,
-                                             split_batch(asmgen.pad4(nacc)))
-        cache[key] = {"text": text, "stats": stats}
-    return cache[key]
+        acc_c = opt.optimize(fp.accumulate_circuit(wE, wa, rnd=r))
+        prod_c = opt.optimize(fp.product_circuit(wE, wi, wa, rnd=r))
+        try:
+            text, stats = asmgen.split_functions(acc_c, prod_c, nin, nacc,
+                                                 split_batch(asmgen.pad4(nacc)))
+            cache[key] = {"text": text, "stats": stats}
+        except regalloc.AllocError as e:
+            cache[key] = {"text": None, "stats": {"unavailable": str(e)}}
+    return cache[key] if cache[key]["text"] is not None else None
 
 
 def generate(verbose=True):
@@ -107,26 +119,15 @@ def generate(verbose=True):
     files = []
     reg_conv, reg_mul = [], []
     for v in variants.CONV_VARIANTS:
-        wE, wi, wa, wo, act = v
+        wE, wi, wa, wo, act, rnd = v
         tag = variants.conv_tag(v)
-        mac, mac_e = netlist("mac", (wE, wi, wa), cache)
-        epi, _ = netlist("epi", (wE, wa, wo, act), cache)
-        prod, prod_e = netlist("prod", (wE, wi, wa), cache)
-        accum, accum_e = netlist("accum", (wE, wa), cache)
-        sp = split_asm(wE, wi, wa, cache)
-        src = f"""// Generated: convolution variant {tag}. Do not edit.
-#include "kernels.hpp"
-#include "registry.hpp"
-namespace hobflops {{
-namespace conv_{tag} {{
-{cache[mac]['text']}
-{cache[epi]['text']}
-{cache[prod]['text']}
-{cache[accum]['text']}
-{sp['text']}
-struct V {{
-  static constexpr int NIN = {nb(wE, wi)}, NACC = {nb(wE, wa)}, NOUT = {nb(wE, wo)};
-  static constexpr int kBatch = {split_batch(asmgen.pad4(nb(wE, wa)))};
+        mac, mac_e = netlist("mac", (wE, wi, wa), rnd, cache)
+        epi, _ = netlist("epi", (wE, wa, wo, act), rnd, cache)
+        prod, prod_e = netlist("prod", (wE, wi, wa), rnd, cache)
+        accum, accum_e = netlist("accum", (wE, wa), rnd, cache)
+        sp = split_asm(wE, wi, wa, rnd, cache)
+        split_text = sp["text"] if sp else ""
+        split_members = """  static constexpr int kBatch = {batch};
   static constexpr const int* kAccSlot = conv_{tag}::kAccSlot;
   static constexpr const int* kProdSlot = conv_{tag}::kProdSlot;
   static constexpr const int* kWSlot = conv_{tag}::kWSlot;
@@ -142,7 +143,25 @@ struct V {{
                                                        const lds_u32* wrow, lds_u32* entry) {{
     conv_{tag}::product_batch(xw, c, wrow, entry);
   }}
-  static __device__ __forceinline__ void mac(uint32_t (&acc)[NACC], const uint32_t (&w)[NIN],
+""".format(batch=split_batch(asmgen.pad4(nb(wE, wa))), tag=tag) if sp else ""
+        split_launch = f"""  if (algo == kAlgoSplit)
+    hipLaunchKernelGGL(conv2d_split_kernel<conv_{tag}::V>, grid, dim3(2 * kConvBlock), 0, stream,
+                       ifm, w, ofm, p);
+  else
+""" if sp else ""
+        src = f"""// Generated: convolution variant {tag}. Do not edit.
+#include "kernels.hpp"
+#include "registry.hpp"
+namespace hobflops {{
+namespace conv_{tag} {{
+{cache[mac]['text']}
+{cache[epi]['text']}
+{cache[prod]['text']}
+{cache[accum]['text']}
+{split_text}
+struct V {{
+  static constexpr int NIN = {nb(wE, wi)}, NACC = {nb(wE, wa)}, NOUT = {nb(wE, wo)};
+{split_members}  static __device__ __forceinline__ void mac(uint32_t (&acc)[NACC], const uint32_t (&w)[NIN],
                                              const uint32_t (&x)[NIN]) {{ {mac}(acc, w, x); }}
   static __device__ __forceinline__ void mul(const uint32_t (&w)[NIN], const uint32_t (&x)[NIN],
                                              uint32_t (&p)[NACC]) {{ {prod}(w, x, p); }}
@@ -157,21 +176,17 @@ struct V {{
 hipError_t launch_conv_{tag}(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
                               const ConvParams& p, int algo, hipStream_t stream) {{
   dim3 grid((unsigned)((p.P + kConvBlock - 1) / kConvBlock), (unsigned)p.MT);
-  if (algo == kAlgoSplit)
-    hipLaunchKernelGGL(conv2d_split_kernel<conv_{tag}::V>, grid, dim3(2 * kConvBlock), 0, stream,
-                       ifm, w, ofm, p);
-  else
-    hipLaunchKernelGGL(conv2d_kernel<conv_{tag}::V>, grid, dim3(kConvBlock), 0, stream, ifm, w, ofm, p);
+{split_launch}    hipLaunchKernelGGL(conv2d_kernel<conv_{tag}::V>, grid, dim3(kConvBlock), 0, stream, ifm, w, ofm, p);
   return hipGetLastError();
 }}
 }}  // namespace hobflops
 """
         files.append((f"conv_{tag}.hip", src))
-        reg_conv.append((v, tag, mac_e["ops"], prod_e["ops"], accum_e["ops"]))
+        reg_conv.append((v, tag, mac_e["ops"], prod_e["ops"], accum_e["ops"], 1 if sp else 0))
     for v in variants.MULADD_VARIANTS:
-        wE, wi, wa = v
+        wE, wi, wa, rnd = v
         tag = variants.muladd_tag(v)
-        fn, e = netlist("muladd", (wE, wi, wa), cache)
+        fn, e = netlist("muladd", (wE, wi, wa), rnd, cache)
         src = f"""// Generated: element-wise MAC variant {tag}. Do not edit.
 #include "kernels.hpp"
 #include "registry.hpp"
@@ -205,14 +220,14 @@ hipError_t launch_muladd_{tag}(const uint32_t* a, const uint32_t* b, const uint3
         reg.append(f"hipError_t launch_muladd_{tag}(const uint32_t*, const uint32_t*, const uint32_t*, "
                    f"uint32_t*, int64_t, hipStream_t);")
     reg.append("const ConvVariant kConvVariants[] = {")
-    for v, tag, ops, pops, aops in reg_conv:
-        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {v[4]}, {ops}, {pops}, {aops}, "
-                   f"launch_conv_{tag}}},")
+    for v, tag, ops, pops, aops, has_split in reg_conv:
+        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {v[4]}, {v[5]}, {has_split}, {ops}, "
+                   f"{pops}, {aops}, launch_conv_{tag}}},")
     reg.append("};")
     reg.append(f"const int kNumConvVariants = {len(reg_conv)};")
     reg.append("const MuladdVariant kMuladdVariants[] = {")
     for v, tag, ops in reg_mul:
-        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {ops}, launch_muladd_{tag}}},")
+        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {ops}, launch_muladd_{tag}}},")
     reg.append("};")
     reg.append(f"const int kNumMuladdVariants = {len(reg_mul)};")
     reg.append("}  // namespace hobflops")
@@ -232,6 +247,8 @@ hipError_t launch_muladd_{tag}(const uint32_t* a, const uint32_t* b, const uint3
             g = gates[k]
             if "ops" in g:
                 print(f"  {k}: {g['ops']} ops (raw {g['raw_nodes']})")
+            elif "unavailable" in g:
+                print(f"  {k}: no split kernel ({g['unavailable']})")
             else:
                 print(f"  {k}: accum {g['accum']}, mul {g['mul']}")
     return [os.path.join(GEN, n) for n, _ in files]

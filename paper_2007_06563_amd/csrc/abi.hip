@@ -30,18 +30,24 @@ const ConvVariant* find_conv(const hobflops_conv_desc* d) {
   for (int i = 0; i < kNumConvVariants; ++i) {
     const ConvVariant& v = kConvVariants[i];
     if (v.wE == d->in_fmt.wE && v.wF_in == d->in_fmt.wF && v.wF_acc == d->acc_fmt.wF &&
-        v.wF_out == d->out_fmt.wF && v.act == d->act)
+        v.wF_out == d->out_fmt.wF && v.act == d->act && v.round == d->round)
       return &v;
   }
   return nullptr;
 }
 
-const MuladdVariant* find_muladd(hobflops_fmt in, hobflops_fmt acc) {
+const MuladdVariant* find_muladd(hobflops_fmt in, hobflops_fmt acc, int round) {
   for (int i = 0; i < kNumMuladdVariants; ++i) {
     const MuladdVariant& v = kMuladdVariants[i];
-    if (v.wE == in.wE && v.wF_in == in.wF && v.wF_acc == acc.wF && acc.wE == in.wE) return &v;
+    if (v.wE == in.wE && v.wF_in == in.wF && v.wF_acc == acc.wF && acc.wE == in.wE &&
+        v.round == round)
+      return &v;
   }
   return nullptr;
+}
+
+int round_ok(int round) {
+  return round == HOBFLOPS_ROUND_NEAREST_EVEN || round == HOBFLOPS_ROUND_TOWARD_ZERO;
 }
 
 // Shape and format checks shared by conv2d and conv2d_supported.
@@ -56,8 +62,7 @@ int conv_check(const hobflops_conv_desc* d) {
   if (d->acc_fmt.wE != d->in_fmt.wE || d->out_fmt.wE != d->in_fmt.wE) return HOBFLOPS_EINVAL;
   if (d->acc_fmt.wF < d->in_fmt.wF) return HOBFLOPS_EINVAL;
   if (d->act != HOBFLOPS_ACT_NONE && d->act != HOBFLOPS_ACT_RELU) return HOBFLOPS_EINVAL;
-  if (d->round != HOBFLOPS_ROUND_NEAREST_EVEN || d->order != HOBFLOPS_ORDER_KY_KX_C)
-    return HOBFLOPS_EINVAL;
+  if (!round_ok(d->round) || d->order != HOBFLOPS_ORDER_KY_KX_C) return HOBFLOPS_EINVAL;
   if (d->algo != HOBFLOPS_ALGO_AUTO && d->algo != HOBFLOPS_ALGO_FUSED &&
       d->algo != HOBFLOPS_ALGO_SPLIT)
     return HOBFLOPS_EINVAL;
@@ -108,7 +113,9 @@ int hobflops_unpack(const uint32_t* planes, int64_t rows, int64_t len, hobflops_
 }
 
 int hobflops_conv2d_supported(const hobflops_conv_desc* d) {
-  return conv_check(d) == HOBFLOPS_OK && find_conv(d) != nullptr;
+  if (conv_check(d) != HOBFLOPS_OK) return 0;
+  const ConvVariant* v = find_conv(d);
+  return v != nullptr && (d->algo != HOBFLOPS_ALGO_SPLIT || v->has_split);
 }
 
 int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
@@ -118,7 +125,7 @@ int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
   if (!ifm || !w || !ofm) return HOBFLOPS_EINVAL;
   if (!aligned(ifm) || !aligned(w) || !aligned(ofm)) return HOBFLOPS_EALIGN;
   const ConvVariant* v = find_conv(d);
-  if (!v) return HOBFLOPS_EUNSUPPORTED;
+  if (!v || (d->algo == HOBFLOPS_ALGO_SPLIT && !v->has_split)) return HOBFLOPS_EUNSUPPORTED;
   ConvParams p;
   p.N = d->N;
   p.H = d->H;
@@ -143,21 +150,24 @@ int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
     if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return hip_status(e);
     const int64_t chain_waves = (int64_t)((p.P + 63) / 64) * p.MT;
-    algo = chain_waves <= 4 * (int64_t)cus ? HOBFLOPS_ALGO_SPLIT : HOBFLOPS_ALGO_FUSED;
+    algo = chain_waves <= 4 * (int64_t)cus && v->has_split ? HOBFLOPS_ALGO_SPLIT
+                                                           : HOBFLOPS_ALGO_FUSED;
   }
   return hip_status(v->launch(ifm, w, ofm, p, algo == HOBFLOPS_ALGO_SPLIT ? kAlgoSplit : kAlgoFused,
                               (hipStream_t)stream));
 }
 
-int hobflops_muladd_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt) {
-  return fmt_ok(in_fmt) && fmt_ok(acc_fmt) && find_muladd(in_fmt, acc_fmt) != nullptr;
+int hobflops_muladd_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int round) {
+  return fmt_ok(in_fmt) && fmt_ok(acc_fmt) && round_ok(round) &&
+         find_muladd(in_fmt, acc_fmt, round) != nullptr;
 }
 
 int hobflops_muladd(const uint32_t* a, const uint32_t* b, const uint32_t* c, uint32_t* r,
-                    int64_t n, hobflops_fmt in_fmt, hobflops_fmt acc_fmt, void* stream) {
-  if (n < 0 || !fmt_ok(in_fmt) || !fmt_ok(acc_fmt)) return HOBFLOPS_EINVAL;
+                    int64_t n, hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int round,
+                    void* stream) {
+  if (n < 0 || !fmt_ok(in_fmt) || !fmt_ok(acc_fmt) || !round_ok(round)) return HOBFLOPS_EINVAL;
   if (acc_fmt.wE != in_fmt.wE || acc_fmt.wF < in_fmt.wF) return HOBFLOPS_EINVAL;
-  const MuladdVariant* v = find_muladd(in_fmt, acc_fmt);
+  const MuladdVariant* v = find_muladd(in_fmt, acc_fmt, round);
   if (!v) return HOBFLOPS_EUNSUPPORTED;
   if (n == 0) return HOBFLOPS_OK;
   if (!a || !b || !c || !r) return HOBFLOPS_EINVAL;
@@ -165,9 +175,11 @@ int hobflops_muladd(const uint32_t* a, const uint32_t* b, const uint32_t* c, uin
   return hip_status(v->launch(a, b, c, r, (n + 31) / 32, (hipStream_t)stream));
 }
 
-int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int* conv_mac_ops,
-                         int* conv_mul_ops, int* conv_accum_ops, int* muladd_ops) {
+int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int round,
+                         int* conv_mac_ops, int* conv_mul_ops, int* conv_accum_ops,
+                         int* muladd_ops) {
   int found = 0;
+  if (!round_ok(round)) return HOBFLOPS_EINVAL;
   if (conv_mac_ops) *conv_mac_ops = 0;
   if (conv_mul_ops) *conv_mul_ops = 0;
   if (conv_accum_ops) *conv_accum_ops = 0;
@@ -175,15 +187,15 @@ int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int* conv_ma
   for (int i = 0; i < kNumConvVariants; ++i) {
     const ConvVariant& v = kConvVariants[i];
     if (v.wE == in_fmt.wE && v.wF_in == in_fmt.wF && v.wF_acc == acc_fmt.wF &&
-        acc_fmt.wE == in_fmt.wE) {
+        acc_fmt.wE == in_fmt.wE && v.round == round) {
       if (conv_mac_ops) *conv_mac_ops = v.mac_ops;
-      if (conv_mul_ops) *conv_mul_ops = v.mul_ops;
-      if (conv_accum_ops) *conv_accum_ops = v.accum_ops;
+      if (conv_mul_ops) *conv_mul_ops = v.has_split ? v.mul_ops : 0;
+      if (conv_accum_ops) *conv_accum_ops = v.has_split ? v.accum_ops : 0;
       found = 1;
       break;
     }
   }
-  const MuladdVariant* m = find_muladd(in_fmt, acc_fmt);
+  const MuladdVariant* m = find_muladd(in_fmt, acc_fmt, round);
   if (m) {
     if (muladd_ops) *muladd_ops = m->ops;
     found = 1;

@@ -15,6 +15,8 @@ typedef hipError_t (*muladd_launch_fn)(const uint32_t* a, const uint32_t* b, con
 
 struct ConvVariant {
   int wE, wF_in, wF_acc, wF_out, act;
+  int round;      // HOBFLOPS_ROUND_*
+  int has_split;  // the split kernel was generated (its netlists fit the registers)
   int mac_ops;    // VALU bitwise instructions of one fused multiply-add step
   int mul_ops;    // ... of the multiplier alone (split kernel, multiplier waves)
   int accum_ops;  // ... of the accumulating adder alone (split kernel, adder waves)
@@ -23,6 +25,7 @@ struct ConvVariant {
 
 struct MuladdVariant {
   int wE, wF_in, wF_acc;
+  int round;  // HOBFLOPS_ROUND_*
   int ops;  // VALU bitwise instructions of one element-wise MAC
   muladd_launch_fn launch;
 };

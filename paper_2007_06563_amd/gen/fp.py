@@ -88,8 +88,9 @@ def signed_const(value, width):
     return [TRUE if (value >> i) & 1 else FALSE for i in range(width)]
 
 
-def fp_mul(C: Circuit, A, B, wE, wF, wFo, canonical=True):
-    """(wE, wF) x (wE, wF) -> (wE, wFo), rounded once (RNE)."""
+def fp_mul(C: Circuit, A, B, wE, wF, wFo, canonical=True, rnd="rne"):
+    """(wE, wF) x (wE, wF) -> (wE, wFo), rounded once: to nearest, ties to
+    even ("rne"), or toward zero ("rtz": the dropped bits are discarded)."""
     a, b = FP(A, wE, wF), FP(B, wE, wF)
     nan_a, inf_a, zero_a, norm_a = classify(C, a)
     nan_b, inf_b, zero_b, norm_b = classify(C, b)
@@ -106,7 +107,7 @@ def fp_mul(C: Circuit, A, B, wE, wF, wFo, canonical=True):
     rb = C.MUX(n, bit(top - 1 - wFo), bit(top - 2 - wFo))
     st = C.OR(C.OR_all([bit(i) for i in range(0, top - 2 - wFo)]),
               C.AND(n, bit(top - 2 - wFo)))
-    round_up = C.AND(rb, C.OR(st, frac[0]))
+    round_up = C.AND(rb, C.OR(st, frac[0])) if rnd == "rne" else FALSE
     frac, rc = C.increment(frac, round_up)
 
     # exponent Ea + Eb - bias + n + rc in (wE+2)-bit two's complement
@@ -129,8 +130,10 @@ def fp_mul(C: Circuit, A, B, wE, wF, wFo, canonical=True):
     return assemble(C, frac, T[:wE], s, nan, inf, is_norm, canonical)
 
 
-def fp_add(C: Circuit, A, B, wE, wF, canonical=True):
-    """(wE, wF) + (wE, wF) -> (wE, wF), rounded once (RNE)."""
+def fp_add(C: Circuit, A, B, wE, wF, canonical=True, rnd="rne"):
+    """(wE, wF) + (wE, wF) -> (wE, wF), rounded once ("rne" or "rtz"; with
+    the sticky bit as the sum's least significant bit, truncating the computed
+    sum truncates the exact one)."""
     a, b = FP(A, wE, wF), FP(B, wE, wF)
     nan_a, inf_a, zero_a, norm_a = classify(C, a)
     nan_b, inf_b, zero_b, norm_b = classify(C, b)
@@ -186,7 +189,7 @@ def fp_add(C: Circuit, A, B, wE, wF, canonical=True):
     frac = v[W - 1 - wF:W - 1]
     rb = v[W - 2 - wF]
     stk = C.OR_all(v[:W - 2 - wF])
-    round_up = C.AND(rb, C.OR(stk, frac[0]))
+    round_up = C.AND(rb, C.OR(stk, frac[0])) if rnd == "rne" else FALSE
     frac, rc = C.increment(frac, round_up)
 
     # Exponent XE + 1 - L + rc in (wE+2)-bit two's complement.
@@ -209,9 +212,10 @@ def fp_add(C: Circuit, A, B, wE, wF, canonical=True):
     return assemble(C, frac, T[:wE], s, nan, inf, is_norm, canonical)
 
 
-def fp_convert(C: Circuit, A, wE, wFs, wFd, relu=False, canonical=True):
-    """(wE, wFs) -> (wE, wFd): exact widening or RNE narrowing, with an
-    optional ReLU first (NaN stays NaN; any negative value or -0 becomes +0)."""
+def fp_convert(C: Circuit, A, wE, wFs, wFd, relu=False, canonical=True, rnd="rne"):
+    """(wE, wFs) -> (wE, wFd): exact widening or narrowing rounded to nearest
+    even ("rne") or toward zero ("rtz"), with an optional ReLU first (NaN
+    stays NaN; any negative value or -0 becomes +0)."""
     a = FP(A, wE, wFs)
     nan, inf, zero, norm = classify(C, a)
     if wFd >= wFs:
@@ -223,7 +227,7 @@ def fp_convert(C: Circuit, A, wE, wFs, wFd, relu=False, canonical=True):
         rb = a.F[D - 1]
         st = C.OR_all(a.F[:D - 1])
         kept = a.F[D:]
-        round_up = C.AND(rb, C.OR(st, kept[0] if kept else TRUE))
+        round_up = C.AND(rb, C.OR(st, kept[0] if kept else TRUE)) if rnd == "rne" else FALSE
         F, c = C.increment(kept, round_up)
         E, ovf = C.increment(a.E, c)
     s = a.s
@@ -240,26 +244,30 @@ def fp_convert(C: Circuit, A, wE, wFs, wFd, relu=False, canonical=True):
 # ---------------------------------------------------------------------------
 # Whole circuits with named ports.
 
-def mul_circuit(wE, wF, wFo, canonical=True):
-    C = Circuit(f"mul_e{wE}m{wF}_m{wFo}")
+def _sfx(rnd):
+    return "" if rnd == "rne" else "_" + rnd
+
+
+def mul_circuit(wE, wF, wFo, canonical=True, rnd="rne"):
+    C = Circuit(f"mul_e{wE}m{wF}_m{wFo}{_sfx(rnd)}")
     a = C.input("a", nb(wE, wF))
     b = C.input("b", nb(wE, wF))
-    C.output("r", fp_mul(C, a, b, wE, wF, wFo, canonical))
+    C.output("r", fp_mul(C, a, b, wE, wF, wFo, canonical, rnd))
     return C
 
 
-def add_circuit(wE, wF, canonical=True):
-    C = Circuit(f"add_e{wE}m{wF}")
+def add_circuit(wE, wF, canonical=True, rnd="rne"):
+    C = Circuit(f"add_e{wE}m{wF}{_sfx(rnd)}")
     a = C.input("a", nb(wE, wF))
     b = C.input("b", nb(wE, wF))
-    C.output("r", fp_add(C, a, b, wE, wF, canonical))
+    C.output("r", fp_add(C, a, b, wE, wF, canonical, rnd))
     return C
 
 
-def convert_circuit(wE, wFs, wFd, relu=False, canonical=True):
-    C = Circuit(f"cvt_e{wE}m{wFs}_m{wFd}{'_relu' if relu else ''}")
+def convert_circuit(wE, wFs, wFd, relu=False, canonical=True, rnd="rne"):
+    C = Circuit(f"cvt_e{wE}m{wFs}_m{wFd}{'_relu' if relu else ''}{_sfx(rnd)}")
     a = C.input("a", nb(wE, wFs))
-    C.output("r", fp_convert(C, a, wE, wFs, wFd, relu, canonical))
+    C.output("r", fp_convert(C, a, wE, wFs, wFd, relu, canonical, rnd))
     return C
 
 
@@ -269,42 +277,42 @@ def widen(lits, wE, wFs, wFd):
     return [FALSE] * (wFd - wFs) + v.F + v.E + [v.s, v.x0, v.x1]
 
 
-def muladd_circuit(wE, wF, wFacc):
+def muladd_circuit(wE, wF, wFacc, rnd="rne"):
     """r = add(widen(c), mul(a, b)) in (wE, wFacc): the element-wise MAC."""
-    C = Circuit(f"muladd_e{wE}m{wF}_m{wFacc}")
+    C = Circuit(f"muladd_e{wE}m{wF}_m{wFacc}{_sfx(rnd)}")
     a = C.input("a", nb(wE, wF))
     b = C.input("b", nb(wE, wF))
     c = C.input("c", nb(wE, wF))
-    p = fp_mul(C, a, b, wE, wF, wFacc, canonical=False)
-    C.output("r", fp_add(C, widen(c, wE, wF, wFacc), p, wE, wFacc, canonical=True))
+    p = fp_mul(C, a, b, wE, wF, wFacc, canonical=False, rnd=rnd)
+    C.output("r", fp_add(C, widen(c, wE, wF, wFacc), p, wE, wFacc, canonical=True, rnd=rnd))
     return C
 
 
-def product_circuit(wE, wF, wFacc):
+def product_circuit(wE, wF, wFacc, rnd="rne"):
     """p = mul(w, x) for the convolution, non-canonical (feeds only the adder)."""
-    C = Circuit(f"prod_e{wE}m{wF}_m{wFacc}")
+    C = Circuit(f"prod_e{wE}m{wF}_m{wFacc}{_sfx(rnd)}")
     w = C.input("w", nb(wE, wF))
     x = C.input("x", nb(wE, wF))
-    C.output("p", fp_mul(C, w, x, wE, wF, wFacc, canonical=False))
+    C.output("p", fp_mul(C, w, x, wE, wF, wFacc, canonical=False, rnd=rnd))
     return C
 
 
-def accumulate_circuit(wE, wFacc):
+def accumulate_circuit(wE, wFacc, rnd="rne"):
     """acc' = add(acc, p) for the convolution, non-canonical in and out."""
-    C = Circuit(f"accum_e{wE}m{wFacc}")
+    C = Circuit(f"accum_e{wE}m{wFacc}{_sfx(rnd)}")
     acc = C.input("acc", nb(wE, wFacc))
     p = C.input("p", nb(wE, wFacc))
-    C.output("acc", fp_add(C, acc, p, wE, wFacc, canonical=False))
+    C.output("acc", fp_add(C, acc, p, wE, wFacc, canonical=False, rnd=rnd))
     return C
 
 
-def mac_circuit(wE, wF, wFacc):
+def mac_circuit(wE, wF, wFacc, rnd="rne"):
     """acc' = add(acc, mul(w, x)): one step of the convolution's accumulation.
     Intermediate accumulators need not be canonical."""
-    C = Circuit(f"mac_e{wE}m{wF}_m{wFacc}")
+    C = Circuit(f"mac_e{wE}m{wF}_m{wFacc}{_sfx(rnd)}")
     acc = C.input("acc", nb(wE, wFacc))
     w = C.input("w", nb(wE, wF))
     x = C.input("x", nb(wE, wF))
-    p = fp_mul(C, w, x, wE, wF, wFacc, canonical=False)
-    C.output("acc", fp_add(C, acc, p, wE, wFacc, canonical=False))
+    p = fp_mul(C, w, x, wE, wF, wFacc, canonical=False, rnd=rnd)
+    C.output("acc", fp_add(C, acc, p, wE, wFacc, canonical=False, rnd=rnd))
     return C

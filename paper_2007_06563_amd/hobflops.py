@@ -16,7 +16,7 @@ _lib = None
 
 SRC_F32, SRC_CODE_U32 = 0, 1
 ACT_NONE, ACT_RELU = 0, 1
-ROUND_NEAREST_EVEN, ORDER_KY_KX_C = 0, 0
+ROUND_NEAREST_EVEN, ROUND_TOWARD_ZERO, ORDER_KY_KX_C = 0, 1, 0
 ALGO_AUTO, ALGO_FUSED, ALGO_SPLIT = 0, 1, 2
 
 
@@ -61,9 +61,9 @@ def lib():
         L.hobflops_unpack.argtypes = [vp, i64, i64, Fmt, ci, vp, vp]
         L.hobflops_conv2d.argtypes = [vp, vp, vp, ctypes.POINTER(ConvDesc), vp]
         L.hobflops_conv2d_supported.argtypes = [ctypes.POINTER(ConvDesc)]
-        L.hobflops_muladd.argtypes = [vp, vp, vp, vp, i64, Fmt, Fmt, vp]
-        L.hobflops_muladd_supported.argtypes = [Fmt, Fmt]
-        L.hobflops_netlist_ops.argtypes = [Fmt, Fmt] + [ctypes.POINTER(ci)] * 4
+        L.hobflops_muladd.argtypes = [vp, vp, vp, vp, i64, Fmt, Fmt, ci, vp]
+        L.hobflops_muladd_supported.argtypes = [Fmt, Fmt, ci]
+        L.hobflops_netlist_ops.argtypes = [Fmt, Fmt, ci] + [ctypes.POINTER(ci)] * 4
         L.hobflops_status_string.argtypes = [ci]
         L.hobflops_status_string.restype = ctypes.c_char_p
         for name in EXPORTS[:-1]:
@@ -142,9 +142,9 @@ def unpack(planes, rows, length, f, kind="f32", out=None):
 
 
 def conv_desc(N, H, W, C, M, KH, KW, stride, pad, in_fmt, acc_fmt, out_fmt, act=ACT_NONE,
-              algo=ALGO_AUTO):
+              algo=ALGO_AUTO, round=ROUND_NEAREST_EVEN):
     return ConvDesc(N, H, W, C, M, KH, KW, stride, pad, fmt(in_fmt), fmt(acc_fmt), fmt(out_fmt),
-                    act, ROUND_NEAREST_EVEN, ORDER_KY_KX_C, algo)
+                    act, round, ORDER_KY_KX_C, algo)
 
 
 def conv_out_hw(d):
@@ -166,25 +166,26 @@ def conv2d_supported(d):
     return bool(lib().hobflops_conv2d_supported(ctypes.byref(d)))
 
 
-def muladd(a, b, c, n, in_fmt, acc_fmt, out=None):
+def muladd(a, b, c, n, in_fmt, acc_fmt, out=None, round=ROUND_NEAREST_EVEN):
     """Element-wise add(widen(c), mul(a, b)) on flat planes of n elements."""
     in_fmt, acc_fmt = fmt(in_fmt), fmt(acc_fmt)
     if out is None:
         out = torch.empty(plane_shape(1, n, acc_fmt), dtype=torch.int32, device=a.device)
-    _check(lib().hobflops_muladd(_ptr(a), _ptr(b), _ptr(c), _ptr(out), n, in_fmt, acc_fmt,
+    _check(lib().hobflops_muladd(_ptr(a), _ptr(b), _ptr(c), _ptr(out), n, in_fmt, acc_fmt, round,
                                  _stream(a)))
     return out
 
 
-def muladd_supported(in_fmt, acc_fmt):
-    return bool(lib().hobflops_muladd_supported(fmt(in_fmt), fmt(acc_fmt)))
+def muladd_supported(in_fmt, acc_fmt, round=ROUND_NEAREST_EVEN):
+    return bool(lib().hobflops_muladd_supported(fmt(in_fmt), fmt(acc_fmt), round))
 
 
-def netlist_ops(in_fmt, acc_fmt):
+def netlist_ops(in_fmt, acc_fmt, round=ROUND_NEAREST_EVEN):
     """dict of VALU ops per 32-lane word: conv 'mac' (fused step), 'mul' and 'accum'
     (the split kernel's two roles), element-wise 'muladd'; 0 where not generated."""
     v = [ctypes.c_int() for _ in range(4)]
-    rc = lib().hobflops_netlist_ops(fmt(in_fmt), fmt(acc_fmt), *[ctypes.byref(x) for x in v])
+    rc = lib().hobflops_netlist_ops(fmt(in_fmt), fmt(acc_fmt), round,
+                                    *[ctypes.byref(x) for x in v])
     if rc != 0:
         raise HobflopsError(rc, lib().hobflops_status_string(rc).decode())
     return dict(zip(("mac", "mul", "accum", "muladd"), (x.value for x in v)))

@@ -65,7 +65,7 @@ def test_conv_rejects_bad_descriptors(hf, bad):
 
 
 def test_conv_rejects_round_order_and_algo(hf):
-    for field, value in (("round", 1), ("order", 2), ("algo", 3), ("algo", -1)):
+    for field, value in (("round", 2), ("round", -1), ("order", 2), ("algo", 3), ("algo", -1)):
         d = desc(hf)
         setattr(d, field, value)
         assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -1, field
@@ -81,6 +81,22 @@ def test_conv_null_misaligned_unsupported(hf):
     assert not hf.conv2d_supported(u)
     assert L.hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(u), None) == -2
     assert hf.conv2d_supported(desc(hf))
+    d = desc(hf)
+    d.round = hf.ROUND_TOWARD_ZERO
+    assert hf.conv2d_supported(d)
+
+
+def test_split_kernel_availability(hf):
+    """Variants whose netlists do not fit the split kernel's registers refuse
+    SPLIT explicitly and still run FUSED (and AUTO)."""
+    wide = dict(in_fmt=(5, 10), acc_fmt=(5, 21), out_fmt=(5, 21))
+    assert hf.conv2d_supported(desc(hf, **wide, algo=hf.ALGO_FUSED))
+    assert hf.conv2d_supported(desc(hf, **wide, algo=hf.ALGO_AUTO))
+    assert not hf.conv2d_supported(desc(hf, **wide, algo=hf.ALGO_SPLIT))
+    d = desc(hf, **wide, algo=hf.ALGO_SPLIT)
+    assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -2
+    assert hf.netlist_ops((5, 10), (5, 21))["mul"] == 0
+    assert hf.conv2d_supported(desc(hf, algo=hf.ALGO_SPLIT))
 
 
 def test_pack_unpack_argument_checks(hf):
@@ -98,12 +114,14 @@ def test_pack_unpack_argument_checks(hf):
 def test_muladd_argument_checks(hf):
     L = hf.lib()
     a = hf.Fmt(5, 3)
-    assert L.hobflops_muladd(FAKE, FAKE, FAKE, FAKE, -5, a, hf.Fmt(5, 4), None) == -1
-    assert L.hobflops_muladd(FAKE, FAKE, FAKE, FAKE, 64, a, hf.Fmt(4, 4), None) == -1
-    assert L.hobflops_muladd(FAKE, FAKE, FAKE, FAKE, 64, a, hf.Fmt(5, 9), None) == -2
-    assert L.hobflops_muladd(FAKE, FAKE, None, FAKE, 64, a, hf.Fmt(5, 4), None) == -1
-    assert L.hobflops_muladd(FAKE, FAKE, FAKE, MISALIGNED, 64, a, hf.Fmt(5, 4), None) == -3
+    assert L.hobflops_muladd(FAKE, FAKE, FAKE, FAKE, -5, a, hf.Fmt(5, 4), 0, None) == -1
+    assert L.hobflops_muladd(FAKE, FAKE, FAKE, FAKE, 64, a, hf.Fmt(4, 4), 0, None) == -1
+    assert L.hobflops_muladd(FAKE, FAKE, FAKE, FAKE, 64, a, hf.Fmt(5, 4), 2, None) == -1
+    assert L.hobflops_muladd(FAKE, FAKE, FAKE, FAKE, 64, a, hf.Fmt(5, 9), 0, None) == -2
+    assert L.hobflops_muladd(FAKE, FAKE, None, FAKE, 64, a, hf.Fmt(5, 4), 0, None) == -1
+    assert L.hobflops_muladd(FAKE, FAKE, FAKE, MISALIGNED, 64, a, hf.Fmt(5, 4), 0, None) == -3
     assert hf.muladd_supported((5, 3), (5, 4))
+    assert hf.muladd_supported((5, 3), (5, 4), hf.ROUND_TOWARD_ZERO)
     assert not hf.muladd_supported((5, 3), (5, 9))
 
 
@@ -111,6 +129,10 @@ def test_netlist_ops_and_status_strings(hf):
     ops = hf.netlist_ops((5, 3), (5, 4))
     assert 50 < ops["mac"] < 1000 and 50 < ops["muladd"] < 1000
     assert 20 < ops["mul"] < ops["mac"] and 50 < ops["accum"] < ops["mac"]
+    # toward zero drops the rounding logic: fewer instructions (paper Sec. 4)
+    rtz = hf.netlist_ops((5, 3), (5, 4), hf.ROUND_TOWARD_ZERO)
+    assert rtz["mac"] < ops["mac"] and rtz["accum"] < ops["accum"]
+    assert rtz["muladd"] < ops["muladd"]
     with pytest.raises(hf.HobflopsError):
         hf.netlist_ops((5, 3), (5, 9))
     L = hf.lib()

@@ -78,15 +78,15 @@ def test_empty_pack_is_a_no_op():
 @pytest.mark.parametrize("v", variants.MULADD_VARIANTS, ids=variants.muladd_tag)
 def test_muladd_vs_oracle(v):
     hf = need_gpu()
-    wE, wi, wa = v
+    wE, wi, wa, rnd = v
     n = (1 << 15) + 77  # ragged tail
     a, b, c = (rand_f32(1000 * wi + t, n) for t in range(3))
     say(f"muladd {v} n={n}")
     pa, pb, pc = (hf.pack(dev(t), (wE, wi)) for t in (a, b, c))
-    r = hf.muladd(pa, pb, pc, n, (wE, wi), (wE, wa))
+    r = hf.muladd(pa, pb, pc, n, (wE, wi), (wE, wa), round=rnd)
     got = codes_of(hf.unpack(r, 1, n, (wE, wa), kind="code"))[0]
     qa, qb, qc = (orc.quantize_f32(t, wE, wi) for t in (a, b, c))
-    want = orc.muladd(qa, qb, qc, wE, wi, wa)
+    want = orc.muladd(qa, qb, qc, wE, wi, wa, rnd=rnd)
     bad = np.flatnonzero(got != want)
     assert bad.size == 0, f"{bad.size} mismatches; first a={qa[bad[0]]:#x} b={qb[bad[0]]:#x} " \
                           f"c={qc[bad[0]]:#x} got={got[bad[0]]:#x} want={want[bad[0]]:#x}"
@@ -96,24 +96,25 @@ def test_muladd_vs_oracle(v):
 def test_muladd_raw_codes_vs_oracle(v):
     """Non-canonical inputs: every field bit random, specials with garbage fields."""
     hf = need_gpu()
-    wE, wi, wa = v
+    wE, wi, wa, rnd = v
     nbits = 3 + wE + wi
     n = 1 << 14
     a, b, c = (I.random_codes(nbits * 10 + t, (1, n), nbits) for t in range(3))
     say(f"muladd raw codes {v}")
     pa, pb, pc = (hf.pack(dev(t.view(np.int32)), (wE, wi)) for t in (a, b, c))
-    r = hf.muladd(pa, pb, pc, n, (wE, wi), (wE, wa))
+    r = hf.muladd(pa, pb, pc, n, (wE, wi), (wE, wa), round=rnd)
     got = codes_of(hf.unpack(r, 1, n, (wE, wa), kind="code"))[0]
     want = orc.muladd(a[0].astype(np.uint64), b[0].astype(np.uint64), c[0].astype(np.uint64), wE,
-                      wi, wa)
+                      wi, wa, rnd=rnd)
     assert np.array_equal(got, want)
 
 
-def run_conv(hf, ifm_codes, w_codes, stride, pad, wE, wi, wa, wo, act, algo=0):
+def run_conv(hf, ifm_codes, w_codes, stride, pad, wE, wi, wa, wo, act, algo=0, rnd=0):
     """GPU conv on code tensors (NHWC / HWIO) -> output codes [N, OH, OW, M]."""
     N, H, W, C = ifm_codes.shape
     KH, KW, _, M = w_codes.shape
-    d = hf.conv_desc(N, H, W, C, M, KH, KW, stride, pad, (wE, wi), (wE, wa), (wE, wo), act, algo)
+    d = hf.conv_desc(N, H, W, C, M, KH, KW, stride, pad, (wE, wi), (wE, wa), (wE, wo), act, algo,
+                     round=rnd)
     OH, OW = hf.conv_out_hw(d)
     pi = hf.pack(dev(ifm_codes.astype(np.uint32).view(np.int32).reshape(N * H * W, C)), (wE, wi))
     pw = hf.pack(dev(w_codes.astype(np.uint32).view(np.int32).reshape(KH * KW * C, M)), (wE, wi))
@@ -140,16 +141,20 @@ def test_conv_variants_vs_oracle(v, algo):
     """Every generated variant, in both kernel shapes, on a problem spanning two
     channel words and two kernel words, both ragged, with padding and specials."""
     hf = need_gpu()
-    wE, wi, wa, wo, act = v
-    g = np.random.default_rng([11, wi, wa, wo, act])
+    wE, wi, wa, wo, act, rnd = v
+    d0 = hf.conv_desc(1, 3, 3, 1, 1, 1, 1, 1, 0, (wE, wi), (wE, wa), (wE, wo), act, algo, round=rnd)
+    if not hf.conv2d_supported(d0):
+        assert algo == hf.ALGO_SPLIT and hf.netlist_ops((wE, wi), (wE, wa), rnd)["mul"] == 0
+        pytest.skip("variant generated without the split kernel (registers)")
+    g = np.random.default_rng([11, wi, wa, wo, act, rnd])
     N, H, W, C, M = 2, 7, 9, 37, 40
     ifm = I.inject_specials(g.uniform(-2, 2, (N, H, W, C)).astype(np.float32), g, 0.01)
     w = I.inject_specials(g.uniform(-1, 1, (3, 3, C, M)).astype(np.float32), g, 0.005)
     qi, qw = orc.quantize_f32(ifm, wE, wi), orc.quantize_f32(w, wE, wi)
     for stride, pad in ((1, 1), (2, 0)):
         say(f"conv variant {v} algo={algo} stride={stride} pad={pad}")
-        got = run_conv(hf, qi, qw, stride, pad, wE, wi, wa, wo, act, algo)
-        want = orc.conv2d(qi, qw, stride, pad, wE, wi, wa, wo, act)
+        got = run_conv(hf, qi, qw, stride, pad, wE, wi, wa, wo, act, algo, rnd)
+        want = orc.conv2d(qi, qw, stride, pad, wE, wi, wa, wo, act, rnd=rnd)
         bad = np.argwhere(got != want)
         assert bad.size == 0, f"{len(bad)} mismatches, first at {bad[0]}"
 

@@ -49,6 +49,17 @@ def random_codes(g, n, wE, wF):
     return c
 
 
+_OPT = {}
+
+
+def optimized(kind, *args, **kw):
+    """opt.optimize of a circuit builder's output, once per session."""
+    key = (kind, args, tuple(sorted(kw.items())))
+    if key not in _OPT:
+        _OPT[key] = opt.optimize(getattr(fp, kind)(*args, **kw))
+    return _OPT[key]
+
+
 def run(C, **ins):
     planes = {}
     for grp, lits in C.inputs:
@@ -63,64 +74,68 @@ N = 1 << 14
 @pytest.mark.parametrize("v", variants.CONV_VARIANTS, ids=variants.conv_tag)
 def test_conv_step_circuits(v):
     """Product, accumulating adder and fused step of every conv variant."""
-    wE, wi, wa, wo, act = v
-    g = np.random.default_rng([7, wE, wi, wa])
+    wE, wi, wa, wo, act, rnd = v
+    r = variants.RND_NAME[rnd]
+    g = np.random.default_rng([7, wE, wi, wa, rnd])
     w, x = random_codes(g, N, wE, wi), random_codes(g, N, wE, wi)
     acc = random_codes(g, N, wE, wa)
-    p_ref = oracle.mul(w, x, wE, wi, wa)
-    a_ref = oracle.add(acc, p_ref, wE, wa)
-    p = run(opt.optimize(fp.product_circuit(wE, wi, wa)), w=w, x=x)["p"]
+    p_ref = oracle.mul(w, x, wE, wi, wa, rnd=rnd)
+    a_ref = oracle.add(acc, p_ref, wE, wa, rnd=rnd)
+    p = run(optimized("product_circuit", wE, wi, wa, rnd=r), w=w, x=x)["p"]
     assert np.array_equal(canon(p, wE, wa), canon(p_ref, wE, wa))
     # the adder reads the product exactly as the multiplier leaves it
-    a = run(opt.optimize(fp.accumulate_circuit(wE, wa)), acc=acc, p=p)["acc"]
+    a = run(optimized("accumulate_circuit", wE, wa, rnd=r), acc=acc, p=p)["acc"]
     assert np.array_equal(canon(a, wE, wa), canon(a_ref, wE, wa))
-    m = run(opt.optimize(fp.mac_circuit(wE, wi, wa)), acc=acc, w=w, x=x)["acc"]
+    m = run(optimized("mac_circuit", wE, wi, wa, rnd=r), acc=acc, w=w, x=x)["acc"]
     assert np.array_equal(canon(m, wE, wa), canon(a_ref, wE, wa))
 
 
 @pytest.mark.parametrize("v", variants.CONV_VARIANTS, ids=variants.conv_tag)
 def test_epilogue_circuits(v):
     """ReLU + convert of the accumulator into the output format: canonical."""
-    wE, wi, wa, wo, act = v
-    g = np.random.default_rng([8, wE, wa, wo, act])
+    wE, wi, wa, wo, act, rnd = v
+    g = np.random.default_rng([8, wE, wa, wo, act, rnd])
     acc = random_codes(g, N, wE, wa)
     want = oracle.relu(acc, wE, wa) if act else acc
-    want = oracle.convert(want, wE, wa, wo)
-    C = opt.optimize(fp.convert_circuit(wE, wa, wo, relu=bool(act)))
+    want = oracle.convert(want, wE, wa, wo, rnd=rnd)
+    C = optimized("convert_circuit", wE, wa, wo, relu=bool(act), rnd=variants.RND_NAME[rnd])
     got = run(C, a=acc)["r"]
     assert np.array_equal(got, want)
 
 
 @pytest.mark.parametrize("v", variants.MULADD_VARIANTS, ids=variants.muladd_tag)
 def test_muladd_circuits(v):
-    wE, wi, wa = v
-    g = np.random.default_rng([9, wE, wi, wa])
+    wE, wi, wa, rnd = v
+    g = np.random.default_rng([9, wE, wi, wa, rnd])
     a, b, c = (random_codes(g, N, wE, wi) for _ in range(3))
-    want = oracle.muladd(a, b, c, wE, wi, wa)
-    got = run(opt.optimize(fp.muladd_circuit(wE, wi, wa)), a=a, b=b, c=c)["r"]
+    want = oracle.muladd(a, b, c, wE, wi, wa, rnd=rnd)
+    got = run(optimized("muladd_circuit", wE, wi, wa, rnd=variants.RND_NAME[rnd]), a=a, b=b, c=c)["r"]
     assert np.array_equal(got, want)
 
 
-def test_small_adder_every_pair():
+@pytest.mark.parametrize("rnd", [variants.RNE, variants.RTZ], ids=["rne", "rtz"])
+def test_small_adder_every_pair(rnd):
     """Every pair of (4,2) codes (512 x 512) through the optimised adder."""
     wE, wF = 4, 2
     nb = nbits(wE, wF)
     allc = np.arange(1 << nb, dtype=np.uint64)
     a = np.repeat(allc, 1 << nb)
     b = np.tile(allc, 1 << nb)
-    want = oracle.add(a, b, wE, wF)
-    got = run(opt.optimize(fp.accumulate_circuit(wE, wF)), acc=a, p=b)["acc"]
+    want = oracle.add(a, b, wE, wF, rnd=rnd)
+    got = run(optimized("accumulate_circuit", wE, wF, rnd=variants.RND_NAME[rnd]), acc=a, p=b)["acc"]
     assert np.array_equal(canon(got, wE, wF), canon(want, wE, wF))
 
 
-def test_small_multiplier_every_pair():
-    wE, wF, wFo = 4, 2, 3
+@pytest.mark.parametrize("rnd", [variants.RNE, variants.RTZ], ids=["rne", "rtz"])
+@pytest.mark.parametrize("wFo", [3, 5])
+def test_small_multiplier_every_pair(rnd, wFo):
+    wE, wF = 4, 2
     nb = nbits(wE, wF)
     allc = np.arange(1 << nb, dtype=np.uint64)
     a = np.repeat(allc, 1 << nb)
     b = np.tile(allc, 1 << nb)
-    want = oracle.mul(a, b, wE, wF, wFo)
-    got = run(opt.optimize(fp.product_circuit(wE, wF, wFo)), w=a, x=b)["p"]
+    want = oracle.mul(a, b, wE, wF, wFo, rnd=rnd)
+    got = run(optimized("product_circuit", wE, wF, wFo, rnd=variants.RND_NAME[rnd]), w=a, x=b)["p"]
     assert np.array_equal(canon(got, wE, wFo), canon(want, wE, wFo))
 
 
