@@ -125,7 +125,7 @@ def _conv_ops(d):
     P = d.N * hf.conv_out_hw(d)[0] * hf.conv_out_hw(d)[1]
     chain_waves = ((P + 63) // 64) * ((d.M + 31) // 32)
     algo = hf.ALGO_SPLIT if chain_waves <= 4 * cus else hf.ALGO_FUSED
-    ops = hf.netlist_ops((d.in_fmt.wE, d.in_fmt.wF), (d.acc_fmt.wE, d.acc_fmt.wF))
+    ops = hf.netlist_ops((d.in_fmt.wE, d.in_fmt.wF), (d.acc_fmt.wE, d.acc_fmt.wF), d.round)
     return algo, (ops["mul"] + ops["accum"] if algo == hf.ALGO_SPLIT else ops["mac"])
 
 
@@ -215,6 +215,48 @@ def suite(reps):
                      "frac": total_ops / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
 
 
+def sweep(reps):
+    """The paper's type sweep (Table 3, Sec. 4): every generated MAC type,
+    single and extended, rounding to nearest even and toward zero, on the
+    MobileNets-shaped layer at batch 1 (the paper's shape) and batch 64; one
+    JSON line each with the netlist gate counts (VALU instructions per 32-MAC
+    word, the analogue of the paper's cell counts)."""
+    from paper_2007_06563_amd import variants as V
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    names = {(4, 3): "HOBFLOPSIEEE8"}
+    names.update({(5, m): f"HOBFLOPS{m + 6}" for m in range(2, 11)})
+    for wE, wi, wa, wo, act, rnd in V.CONV_VARIANTS:
+        if act or (wE, wi) not in names:
+            continue
+        ext = wa == 2 * wi + 1 and wa != wi + 1
+        tname = names[(wE, wi)] + ("e" if ext else "")
+        ops = hf.netlist_ops((wE, wi), (wE, wa), rnd)
+        for batch in (1, 64):
+            s = I.mobilenet_layer(batch)
+            ifm, w = I.conv_inputs(I.TYPE_SWEEP, 0, s)
+            d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, (wE, wi),
+                             (wE, wa), (wE, wo), round=rnd)
+            pi = hf.pack(torch.from_numpy(ifm.reshape(-1, s.C)).to(dev), (wE, wi))
+            pw = hf.pack(torch.from_numpy(w.reshape(-1, s.M)).to(dev), (wE, wi))
+            o = hf.conv2d(pi, pw, d)
+            ms = _time(lambda: hf.conv2d(pi, pw, d, out=o), reps, stream)
+            algo, G = _conv_ops(d)
+            if G == 0:  # no split kernel for this type: the library ran the fused one
+                algo, G = hf.ALGO_FUSED, ops["mac"]
+            lane_ops = s.macs / 32.0 * G
+            print(json.dumps({
+                "type": tname, "in": [wE, wi], "acc": [wE, wa], "round": V.RND_NAME[rnd],
+                "gates": {"mac": ops["mac"], "mul": ops["mul"], "accum": ops["accum"],
+                          "muladd": ops["muladd"]},
+                "workload": f"conv {s.N}x{s.H}x{s.W}x{s.C} -> {s.M} 3x3 s2 p1",
+                "kernel": "split" if algo == hf.ALGO_SPLIT else "fused", "ms": ms,
+                "gmacs": s.macs / (ms * 1e-3) / 1e9,
+                "roofline": {"bound": "alu", "achieved": lane_ops / (ms * 1e-3) / 1e12,
+                             "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
+                             "frac": lane_ops / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -228,6 +270,9 @@ def main():
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB "
                          "(steps times): the reference for scaling HBM byte counters")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the one-line benchmark: the paper's MAC type sweep on the "
+                         "MobileNets-shaped layer, one JSON line per type, rounding and batch")
     ap.add_argument("--suite", action="store_true",
                     help="instead of the one-line benchmark: one JSON line per further workload "
                          "(element-wise sweep, mantissa sweep, 13-layer stack)")
@@ -241,6 +286,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.suite:
         suite(args.steps)
+        return
+    if args.sweep:
+        sweep(args.steps)
         return
     if args.calibrate_copy_mib:
         n = args.calibrate_copy_mib * (1 << 20) // 4

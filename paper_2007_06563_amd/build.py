@@ -83,10 +83,16 @@ def netlist(kind, key, rnd, cache):
     return fname, entry
 
 
-def split_batch(naccp):
+# Product ring depth and load schedule of the split kernel's accumulator role
+# (see gen/asmgen.split_functions).
+SPLIT_SLOTS, SPLIT_SCHEDULE = 2, "batch"
+
+
+def split_batch(naccp, slots=None):
     """Products per barrier in the split kernel: even, and the LDS product
-    ring of 2 halves x batch x 256 lanes x entry words within 128 KiB."""
-    return 4 if 2 * 4 * 256 * naccp * 4 <= 128 * 1024 else 2
+    ring of slots x batch x 256 lanes x entry words within 144 KiB."""
+    slots = slots or SPLIT_SLOTS
+    return 4 if slots * 4 * 256 * naccp * 4 <= 144 * 1024 else 2
 
 
 def split_asm(wE, wi, wa, rnd, cache):
@@ -100,7 +106,8 @@ def split_asm(wE, wi, wa, rnd, cache):
         prod_c = opt.optimize(fp.product_circuit(wE, wi, wa, rnd=r))
         try:
             text, stats = asmgen.split_functions(acc_c, prod_c, nin, nacc,
-                                                 split_batch(asmgen.pad4(nacc)))
+                                                 split_batch(asmgen.pad4(nacc)),
+                                                 SPLIT_SLOTS, SPLIT_SCHEDULE)
             cache[key] = {"text": text, "stats": stats}
         except regalloc.AllocError as e:
             cache[key] = {"text": None, "stats": {"unavailable": str(e)}}
@@ -131,9 +138,11 @@ def generate(verbose=True):
   static constexpr const int* kAccSlot = conv_{tag}::kAccSlot;
   static constexpr const int* kProdSlot = conv_{tag}::kProdSlot;
   static constexpr const int* kWSlot = conv_{tag}::kWSlot;
+  static constexpr int kSlots = conv_{tag}::kSlots;
   static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[(NACC + 3) & ~3],
-                                                    const lds_u32* e0, const lds_u32* e1, int nb) {{
-    conv_{tag}::accum_loop(acc, e0, e1, nb);
+                                                    const lds_u32* e0, const lds_u32* e1,
+                                                    const lds_u32* e2, int nb) {{
+    conv_{tag}::accum_loop(acc, e0, e1, e2, nb);
   }}
   static __device__ __forceinline__ void product_step(const uint32_t (&xw)[NIN], int c,
                                                       const lds_u32* wrow, lds_u32* entry) {{

@@ -217,11 +217,13 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   constexpr int NINP = (NIN + 3) & ~3;    // weight row stride in LDS (16-byte aligned)
   constexpr int NACCP = (NACC + 3) & ~3;  // product entry per lane (16-byte aligned)
   constexpr int K = V::kBatch;
+  constexpr int S = V::kSlots;        // product ring depth: batches in flight
   constexpr int kStride = NACCP / 4;  // uint4 per product entry
   static_assert(K % 2 == 0, "the accumulator ping-pong needs an even batch");
+  static_assert(S == 2 || S == 3, "ring of two or three batches");
   static_assert(K * NIN <= kConvBlock, "one weight word per multiplier thread");
-  static_assert(2 * K * 256 * NACCP * 4 <= 128 * 1024, "product ring exceeds the LDS budget");
-  __shared__ uint4 pring[2 * K * 4 * 64 * kStride];  // [half][k][wave][lane][kStride]
+  static_assert(S * K * 256 * NACCP * 4 <= 144 * 1024, "product ring exceeds the LDS budget");
+  __shared__ uint4 pring[S * K * 4 * 64 * kStride];  // [slot][k][wave][lane][kStride]
   __shared__ uint4 wring[3 * K * NINP / 4];          // [slot][k][NINP words]
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -241,9 +243,9 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   const int T = p.KH * p.KW * p.C;  // taps per output
   const int nb = (T + K - 1) / K;
 
-  auto entry = [&](int b, int k) {  // batch b lives in ring half b % 2
+  auto entry = [&](int b, int k) {  // batch b lives in ring slot b % S
     // C-style cast: generic pointer into the LDS address space
-    return (lds_u32*)(pring + ((((size_t)(b & 1) * K + k) * 4 + pw) * 64 + lane) * kStride);
+    return (lds_u32*)(pring + ((((size_t)(b % S) * K + k) * 4 + pw) * 64 + lane) * kStride);
   };
 
   // ---- multiplier waves: weight staging (thread t of the 256 loads word t)
@@ -322,12 +324,16 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
 #pragma unroll
   for (int s = 0; s < NACCP; ++s) acc[s] = 0u;  // +0
 
-  // Schedule, one barrier per step i = -1 .. nb-1: the multiplier waves make
-  // batch i+1 (into ring half (i+1) % 2) and stage the weights of batch i+3
-  // (into weight slot i % 3, last read at step i-2); the accumulator waves add
-  // batch i, complete since the barrier of step i-1. Half i % 2 is rewritten
-  // at step i+1, after the accumulators' last read of it.
-  // Each role runs its own loop with the same number of barriers (nb + 2),
+  // Schedule, one barrier per step i = -(S-1) .. nb-1: the multiplier waves
+  // make batch i+S-1 (into ring slot (i+S-1) % S) and stage the weights of
+  // batch i+3 (into weight slot i % 3, last read at step i-S+1 < i); the
+  // accumulator waves add batch i, complete since the barrier of step i-1,
+  // and with a three-slot ring may read batch i+1 (complete since step i-1)
+  // before the barrier. Slot i % S is rewritten at step i+1, after the
+  // accumulators' last read of it (loads of it still in flight at the
+  // barrier are of batch i+1 < i+S only when S = 3, and land in slot
+  // (i+1) % 3, which step i+1 does not write).
+  // Each role runs its own loop with the same number of barriers (nb + S),
   // so that the multiplier's register use never meets the accumulator's
   // loop-carried planes. The multiplier waves issue at raised priority: their
   // instruction stream stalls on LDS traffic, and without priority the
@@ -337,22 +343,23 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   if (mul_role) {
     __builtin_amdgcn_s_setprio(3);
     load_ifm(0, 0, 0);
-    fetch_w(0);
-    store_w(0);
-    fetch_w(1);
-    store_w(1);
+#pragma unroll
+    for (int j = 0; j <= 3 - S; ++j) {  // weights stored before the first step
+      fetch_w(j);
+      store_w(j);
+    }
     __syncthreads();
-    for (int i = -1; i < nb; ++i) {
+    for (int i = 1 - S; i < nb; ++i) {
       fetch_w(i + 3);
-      if (i + 1 < nb) produce(i + 1);
+      if (i + S - 1 < nb) produce(i + S - 1);
       store_w(i + 3);
       __syncthreads();
     }
     return;
   }
-  __syncthreads();
-  __syncthreads();
-  V::accum_loop(acc, entry(0, 0), entry(1, 0), nb);  // nb barriers
+#pragma unroll
+  for (int j = 0; j < S; ++j) __syncthreads();
+  V::accum_loop(acc, entry(0, 0), entry(1, 0), entry(S - 1, 0), nb);  // nb barriers
   if (!active) return;
   uint32_t planes[NACC], out[NOUT];
 #pragma unroll

@@ -4,16 +4,14 @@ The two wave roles of the split kernel run their netlists as inline assembly
 with explicit registers chosen by gen.regalloc, so that no VALU instruction
 reads two VGPRs of one bank (see gen/regalloc.py). The functions produced:
 
-* ``accum_loop(acc, e0, e1, nb)``: the whole accumulator role. Batch b (K
-  products) sits in half b % 2 of the LDS product ring; after each barrier
-  the K entries are requested with 16-byte loads at immediate offsets from
-  this lane's first entry, and K copies of the adder netlist add them into the
-  accumulator, each waiting for its own entry only. The accumulator
-  ping-pongs between two register sets and is back in the first after the
-  batch (K is even). ``acc`` holds the accumulator planes in register-slot
-  order; kAccSlot[b] is the slot of plane b. (Requesting the next batch's
-  entries before the barrier, from a third ring slot, was measured slower:
-  the early loads compete with the multiplier's stores.)
+* ``accum_loop(acc, e0, e1, e2, nb)``: the whole accumulator role. Batch b
+  (K products) sits in slot b % kSlots of the LDS product ring; its entries
+  are requested with 16-byte loads at immediate offsets from this lane's first
+  entry, on the schedule split_functions is given, and K copies of the adder
+  netlist add them into the accumulator, each waiting for its own entry only.
+  The accumulator ping-pongs between two register sets and is back in the
+  first after the batch (K is even). ``acc`` holds the accumulator planes in
+  register-slot order; kAccSlot[b] is the slot of plane b.
 * ``product_batch(xw, c, wrow, entry)``: the K products of one batch whose
   taps c .. c+K-1 lie in one IFM channel word: all K weight rows are requested
   from the LDS weight ring first (plane b in word kWSlot[b]); per product, bit
@@ -51,9 +49,17 @@ def _asm_string(lines):
     return "\n".join(f'      "{ln}\\n"' for ln in lines)
 
 
-def split_functions(accum_C, prod_C, nin, nacc, K):
+def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch"):
     """C++ text (inside a variant's namespace) of the two asm functions and
-    their slot tables, plus allocation statistics."""
+    their slot tables, plus allocation statistics.
+
+    slots: LDS product ring depth (batches in flight; the multiplier runs
+    slots-1 batches ahead). schedule: "batch" requests all K entries of a
+    batch after its barrier; "step" requests entry k+1 before adding entry k;
+    "prefetch" (slots 3) is "step" plus entry 0 of the next batch requested
+    before the last add of the current one."""
+    assert slots in (2, 3) and schedule in ("batch", "step", "prefetch")
+    assert schedule != "prefetch" or slots == 3
     ninp, naccp = pad4(nin), pad4(nacc)
     kstride = naccp // 4
     A = list(range(BASE, BASE + naccp))
@@ -66,46 +72,80 @@ def split_functions(accum_C, prod_C, nin, nacc, K):
     prod_slot = [r - P[0][0] for r in place["in"]["p"]]
     entry_bytes = 4 * 64 * kstride * 16  # ring distance between batch entries k and k+1
 
-    def batch(half):
-        """One batch from ring half `half`: all K entries are requested after
-        the barrier, and the adder for entry k waits for entry k only."""
-        out = [f"ds_read_b128 v[{P[k][4 * j]}:{P[k][4 * j] + 3}], %[e{half}] "
-               f"offset:{k * entry_bytes + 16 * j}" for k in range(K) for j in range(kstride)]
-        for k in range(K):
-            out.append(f"s_waitcnt lgkmcnt({(K - 1 - k) * kstride})")
-            m = {}
-            if k % 2 == 1:  # B -> A
-                m.update({a: b for a, b in zip(A, B)})
-                m.update({b: a for a, b in zip(A, B)})
-            m.update({p0: pk for p0, pk in zip(P[0], P[k])})
-            out += _rename(lines, m)
-        return out
+    def reads(slot, k):
+        return [f"ds_read_b128 v[{P[k][4 * j]}:{P[k][4 * j] + 3}], %[e{slot}] "
+                f"offset:{k * entry_bytes + 16 * j}" for j in range(kstride)]
 
-    # A barrier ends each batch. The count is exact: the loop starts with
-    # nothing of the compiler's in flight and ends with nothing of its own.
-    body = ["s_waitcnt lgkmcnt(0)", "s_mov_b32 %[n], %[nb]", "L%=_loop:"]
-    for half in range(2):
-        body += batch(half)
+    def netlist(k):
+        m = {}
+        if k % 2 == 1:  # B -> A
+            m.update({a: b for a, b in zip(A, B)})
+            m.update({b: a for a, b in zip(A, B)})
+        m.update({p0: pk for p0, pk in zip(P[0], P[k])})
+        return _rename(lines, m)
+
+    # Events of one batch in issue order: ("r", slot, k) loads entry k of a
+    # slot, ("n", k) adds entry k of the current slot.
+    def events(slot):
+        nxt = (slot + 1) % slots
+        ev = []
+        if schedule == "batch":
+            ev += [("r", slot, k) for k in range(K)]
+            ev += [("n", k) for k in range(K)]
+        else:
+            if schedule == "step":
+                ev.append(("r", slot, 0))
+            for k in range(K):
+                if k + 1 < K:
+                    ev.append(("r", slot, k + 1))
+                elif schedule == "prefetch":
+                    ev.append(("r", nxt, 0))
+                ev.append(("n", k))
+        return ev
+
+    # The wait before adding entry k leaves in flight only the loads issued
+    # after entry k's (LDS operations complete in order). Loads still in
+    # flight at a barrier are carried across it ("prefetch" only).
+    carried = [("r", 0, 0)] if schedule == "prefetch" else []
+    body = ["s_waitcnt lgkmcnt(0)"]  # nothing of the compiler's in flight: counts below are exact
+    if carried:
+        body += reads(0, 0)
+    body += ["s_mov_b32 %[n], %[nb]", "L%=_loop:"]
+    for slot in range(slots):
+        inflight = list(carried)
+        for e in events(slot):
+            if e[0] == "r":
+                body += reads(e[1], e[2])
+                inflight += [e] * kstride
+            else:
+                k = e[1]
+                last = max(i for i, x in enumerate(inflight) if x == ("r", slot, k))
+                newer = len(inflight) - 1 - last
+                body.append(f"s_waitcnt lgkmcnt({newer})")
+                inflight = inflight[last + 1:]
+                body += netlist(k)
+        carried = inflight
         body += ["s_barrier",
                  "s_sub_u32 %[n], %[n], 1",
                  "s_cmp_eq_u32 %[n], 0",
                  "s_cbranch_scc1 L%=_done"]
-    body += ["s_branch L%=_loop", "L%=_done:"]
+    body += ["s_branch L%=_loop", "L%=_done:", "s_waitcnt lgkmcnt(0)"]
     used = set(B) | set(r for blk in P for r in blk) | set(st_acc["temps"])
     clob = ", ".join(f'"v{r}"' for r in sorted(used))
     state = ", ".join(f'"+{{v{BASE + s}}}"(acc[{s}])' for s in range(naccp))
     accum_fn = f"""static constexpr int kAccSlot[{nacc}] = {{{", ".join(map(str, acc_slot))}}};
 static constexpr int kProdSlot[{nacc}] = {{{", ".join(map(str, prod_slot))}}};
-// The accumulator role: nb batches of K products from the two-half LDS ring
-// (this lane's first entry of half h at e_h, batch b in half b % 2), one
-// barrier after each batch; acc holds the planes in register-slot order.
+static constexpr int kSlots = {slots};
+// The accumulator role: nb batches of K products from the LDS ring of kSlots
+// slots (this lane's first entry of slot s at e_s, batch b in slot b % kSlots),
+// one barrier after each batch; acc holds the planes in register-slot order.
 static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], const lds_u32* e0,
-                                                  const lds_u32* e1, int nb) {{
+                                                  const lds_u32* e1, const lds_u32* e2, int nb) {{
   uint32_t n;
   asm volatile(
 {_asm_string(body)}
       : {state}, [n] "=&s"(n)
-      : [e0] "v"(e0), [e1] "v"(e1), [nb] "s"(nb)
+      : [e0] "v"(e0), [e1] "v"(e1), [e2] "v"(e2), [nb] "s"(nb)
       : {clob}, "scc", "memory");
 }}
 """

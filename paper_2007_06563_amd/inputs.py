@@ -16,7 +16,7 @@ from dataclasses import dataclass
 import numpy as np
 
 # Workload ids used in the seeds.
-SMALL_CONV, FMA_SWEEP, RESNET_CONV, MANTISSA_SWEEP, RESNET_STACK = 0, 1, 2, 3, 4
+SMALL_CONV, FMA_SWEEP, RESNET_CONV, MANTISSA_SWEEP, RESNET_STACK, TYPE_SWEEP = 0, 1, 2, 3, 4, 5
 
 # Formats of the element-wise a*b+c sweep: (wE, wF) of the operands; the result
 # has one more fraction bit (the paper's "single" MAC type, Table 3).
@@ -53,6 +53,14 @@ SMALL_CONV_SHAPE = ConvShape(1, 8, 8, 4, 8, 3, 3, 1, 1)
 RESNET_CONV_SHAPE = ConvShape(8, 56, 56, 64, 64, 3, 3, 1, 1)
 MANTISSA_SWEEP_SHAPES = [ConvShape(4, 224, 224, 3, 64, 3, 3, 1, 1),
                          ConvShape(4, 28, 28, 256, 512, 3, 3, 1, 1)]
+
+
+def mobilenet_layer(batch):
+    """The layer the paper's type sweep runs on (Sec. 3.4 and Sec. 4): the
+    "Conv dw / s2" position of MobileNets, 14x14x512 input, 3x3 kernels,
+    stride 2. Taken here as a dense MCMK conv with M = 512 and pad 1 (the
+    paper gives neither M nor the padding)."""
+    return ConvShape(batch, 14, 14, 512, 512, 3, 3, 2, 1)
 
 
 def resnet_stack_shapes(batch=16):
