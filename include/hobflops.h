@@ -71,6 +71,11 @@ enum { HOBFLOPS_ACT_NONE = 0, HOBFLOPS_ACT_RELU = 1 };
  * same wave; SPLIT runs them on separate waves of the same CU so that a
  * launch with few accumulator chains can still fill the VALU. */
 enum { HOBFLOPS_ALGO_AUTO = 0, HOBFLOPS_ALGO_FUSED = 1, HOBFLOPS_ALGO_SPLIT = 2 };
+/* What hobflops_conv2d writes to ofm: PL32 planes of out_fmt (the next
+ * layer's input, the default), or with the unpack fused into the epilogue
+ * (the last layer, paper Sec. 3.4), one value per element, row-major
+ * [N*OH*OW][M]: float32 as hobflops_unpack writes them, or uint32 codes. */
+enum { HOBFLOPS_OFM_PLANES = 0, HOBFLOPS_OFM_F32 = 1, HOBFLOPS_OFM_CODE_U32 = 2 };
 
 /* Number of uint32 words of a PL32 tensor: rows * ceil(len/32) * NB.
  * Returns HOBFLOPS_OK and writes *words, or HOBFLOPS_EINVAL. */
@@ -99,6 +104,8 @@ int hobflops_unpack(const uint32_t* planes, int64_t rows, int64_t len, hobflops_
  *   ifm: PL32, rows N*H*W (NHWC order), len C, format in_fmt
  *   w:   PL32, rows KH*KW*C (HWIO order, row (ky*KW + kx)*C + c), len M, in_fmt
  *   ofm: PL32, rows N*OH*OW, len M, format out_fmt; OH = (H + 2*pad - KH)/stride + 1
+ *        (ofm_kind HOBFLOPS_OFM_PLANES), or N*OH*OW*M float32 values or uint32
+ *        codes of out_fmt, row-major (HOBFLOPS_OFM_F32 / _CODE_U32)
  * For each output (n, oy, ox, m): acc = +0 in acc_fmt; for ky, then kx, then c:
  *   acc = add(acc, mul(w[ky][kx][c][m], x)), x the IFM value or +0 for a
  *   padding tap, mul rounding into acc_fmt and add rounding in acc_fmt; then
@@ -113,7 +120,8 @@ typedef struct {
   int N, H, W, C, M, KH, KW, stride, pad;
   hobflops_fmt in_fmt, acc_fmt, out_fmt;
   int act, round, order;
-  int algo; /* HOBFLOPS_ALGO_* */
+  int algo;     /* HOBFLOPS_ALGO_* */
+  int ofm_kind; /* HOBFLOPS_OFM_* */
 } hobflops_conv_desc;
 
 int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,

@@ -170,6 +170,7 @@ namespace conv_{tag} {{
 {split_text}
 struct V {{
   static constexpr int NIN = {nb(wE, wi)}, NACC = {nb(wE, wa)}, NOUT = {nb(wE, wo)};
+  static constexpr int wE = {wE}, wF_OUT = {wo};
 {split_members}  static __device__ __forceinline__ void mac(uint32_t (&acc)[NACC], const uint32_t (&w)[NIN],
                                              const uint32_t (&x)[NIN]) {{ {mac}(acc, w, x); }}
   static __device__ __forceinline__ void mul(const uint32_t (&w)[NIN], const uint32_t (&x)[NIN],

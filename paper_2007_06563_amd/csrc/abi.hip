@@ -66,6 +66,9 @@ int conv_check(const hobflops_conv_desc* d) {
   if (d->algo != HOBFLOPS_ALGO_AUTO && d->algo != HOBFLOPS_ALGO_FUSED &&
       d->algo != HOBFLOPS_ALGO_SPLIT)
     return HOBFLOPS_EINVAL;
+  if (d->ofm_kind != HOBFLOPS_OFM_PLANES && d->ofm_kind != HOBFLOPS_OFM_F32 &&
+      d->ofm_kind != HOBFLOPS_OFM_CODE_U32)
+    return HOBFLOPS_EINVAL;
   const int64_t OH = (d->H + 2 * (int64_t)d->pad - d->KH) / d->stride + 1;
   const int64_t OW = (d->W + 2 * (int64_t)d->pad - d->KW) / d->stride + 1;
   const int64_t P = (int64_t)d->N * OH * OW;
@@ -141,6 +144,8 @@ int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
   p.CG = (d->C + 31) / 32;
   p.MT = (d->M + 31) / 32;
   p.P = p.N * p.OH * p.OW;
+  p.ofm_kind = d->ofm_kind;
+  p.ofm_vec = ((uintptr_t)ofm & 15u) == 0;
   int algo = d->algo;
   if (algo == HOBFLOPS_ALGO_AUTO) {
     // one accumulator wave per 64 positions and m-tile; split when they would

@@ -8,6 +8,7 @@
 //
 // A Variant type supplies the generated netlists:
 //   static constexpr int NIN, NACC, NOUT;     planes per value
+//   static constexpr int wE, wF_OUT;          the output format
 //   static __device__ void mac(uint32_t (&acc)[NACC], const uint32_t (&w)[NIN],
 //                              const uint32_t (&x)[NIN]);        acc = acc + w*x
 //   static __device__ void epi(const uint32_t (&acc)[NACC], uint32_t (&out)[NOUT]);
@@ -17,6 +18,9 @@
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "bitmat.hpp"
+#include "codec.hpp"
 
 namespace hobflops {
 
@@ -28,7 +32,79 @@ struct ConvParams {
   int CG;  // ceil(C / 32): channel words per IFM position
   int MT;  // ceil(M / 32): kernel words (m-tiles) per weight row / OFM position
   int P;   // N * OH * OW output positions
+  int ofm_kind;  // kOfmPlanes, kOfmF32 or kOfmCode
+  int ofm_vec;   // ofm is 16-byte aligned (value rows may be stored 16 bytes at a time)
 };
+
+// What the convolution writes (hobflops_conv_desc.ofm_kind): PL32 planes, or
+// per value, row-major [P][M], float32 values or uint32 codes.
+constexpr int kOfmPlanes = 0, kOfmF32 = 1, kOfmCode = 2;
+
+// float32 bit-planes of the 32 values whose (wE, wF) code planes are `c`
+// (F, E, s, x0, x1 from plane 0 up), for wE <= 7, where every value of the
+// format is a normal float32: exponent E + 127 - bias, fraction F << (23 - wF),
+// specials as hobflops_unpack writes them (NaN 0x7FC00000).
+template <int wE, int wF>
+__device__ __forceinline__ void float_planes(const uint32_t* c, uint32_t (&f)[32]) {
+  static_assert(wE <= 7 && wF <= 23, "every value a normal float32");
+  const uint32_t s = c[wF + wE], x0 = c[wF + wE + 1], x1 = c[wF + wE + 2];
+  const uint32_t norm = x0 & ~x1, nan = x0 & x1;
+#pragma unroll
+  for (int b = 0; b < 32; ++b) f[b] = 0u;
+#pragma unroll
+  for (int i = 0; i < wF; ++i) f[23 - wF + i] = norm & c[i];
+  f[22] |= nan;
+  constexpr uint32_t add = 127u - ((1u << (wE - 1)) - 1u);
+  uint32_t carry = 0u;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {  // exponent E + add, bitsliced ripple
+    const uint32_t e = i < wE ? c[wF + i] : 0u;
+    const uint32_t k = ((add >> i) & 1u) ? ~0u : 0u;
+    f[23 + i] = (norm & (e ^ k ^ carry)) | x1;
+    carry = (e & k) | (carry & (e ^ k));
+  }
+  f[31] = s & ~nan;
+}
+
+// The epilogue's store of one lane's output word group: 32 values of one
+// position, kernels 32*mt .. 32*mt+31, as NOUT plane words or, moved out of
+// plane order with one bit-matrix transpose, as codes or float32 values (the
+// decode done on the planes first), 16 bytes per store where the row allows.
+template <int NOUT, int wE, int wF>
+__device__ __forceinline__ void store_ofm(const uint32_t (&out)[NOUT], uint32_t* __restrict__ ofm,
+                                          int pos, int mt, const ConvParams& p) {
+  if (p.ofm_kind == kOfmPlanes) {
+    uint32_t* op = ofm + ((size_t)pos * p.MT + mt) * NOUT;
+#pragma unroll
+    for (int b = 0; b < NOUT; ++b) op[b] = out[b];
+    return;
+  }
+  uint32_t v[32];
+  if (p.ofm_kind == kOfmF32 && wE <= 7) {
+    float_planes<(wE <= 7 ? wE : 7), wF>(out, v);
+    transpose32(v);
+  } else {
+#pragma unroll
+    for (int b = 0; b < 32; ++b) v[b] = b < NOUT ? out[b] : 0u;
+    transpose32(v);
+    if (p.ofm_kind == kOfmF32) {
+#pragma unroll
+      for (int j = 0; j < 32; ++j) v[j] = decode_bits(v[j], wE, wF);
+    }
+  }
+  const int m0 = mt * 32;
+  const int nm = min(32, p.M - m0);
+  uint32_t* op = ofm + (size_t)pos * p.M + m0;
+  if (nm == 32 && (p.M & 3) == 0 && p.ofm_vec) {
+#pragma unroll
+    for (int j = 0; j < 32; j += 4)
+      *reinterpret_cast<uint4*>(op + j) = make_uint4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 32; ++j)
+      if (j < nm) op[j] = v[j];
+  }
+}
 
 constexpr int kConvBlock = 256;  // positions per workgroup: four wave64s
 
@@ -179,9 +255,7 @@ __global__ __launch_bounds__(kConvBlock) void conv2d_kernel(const uint32_t* __re
   if (!active) return;
   uint32_t out[NOUT];
   V::epi(acc, out);
-  uint32_t* op = ofm + ((size_t)pos * p.MT + mt) * NOUT;
-#pragma unroll
-  for (int b = 0; b < NOUT; ++b) op[b] = out[b];
+  store_ofm<NOUT, V::wE, V::wF_OUT>(out, ofm, pos, mt, p);
 }
 
 // MCMK convolution, split shape: multiply and accumulate on different waves.
@@ -365,9 +439,7 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
 #pragma unroll
   for (int bb = 0; bb < NACC; ++bb) planes[bb] = acc[V::kAccSlot[bb]];
   V::epi(planes, out);
-  uint32_t* op = ofm + ((size_t)pos * p.MT + mt) * NOUT;
-#pragma unroll
-  for (int bb = 0; bb < NOUT; ++bb) op[bb] = out[bb];
+  store_ofm<NOUT, V::wE, V::wF_OUT>(out, ofm, pos, mt, p);
 }
 
 // Element-wise r = a*b + c (multiply rounded, then add rounded) on flat PL32

@@ -18,6 +18,7 @@ SRC_F32, SRC_CODE_U32 = 0, 1
 ACT_NONE, ACT_RELU = 0, 1
 ROUND_NEAREST_EVEN, ROUND_TOWARD_ZERO, ORDER_KY_KX_C = 0, 1, 0
 ALGO_AUTO, ALGO_FUSED, ALGO_SPLIT = 0, 1, 2
+OFM_PLANES, OFM_F32, OFM_CODE = 0, 1, 2
 
 
 class HobflopsError(RuntimeError):
@@ -39,7 +40,7 @@ class ConvDesc(ctypes.Structure):
                 ("KW", ctypes.c_int), ("stride", ctypes.c_int), ("pad", ctypes.c_int),
                 ("in_fmt", Fmt), ("acc_fmt", Fmt), ("out_fmt", Fmt),
                 ("act", ctypes.c_int), ("round", ctypes.c_int), ("order", ctypes.c_int),
-                ("algo", ctypes.c_int)]
+                ("algo", ctypes.c_int), ("ofm_kind", ctypes.c_int)]
 
 
 EXPORTS = ("hobflops_plane_words", "hobflops_pack", "hobflops_unpack", "hobflops_conv2d",
@@ -142,9 +143,9 @@ def unpack(planes, rows, length, f, kind="f32", out=None):
 
 
 def conv_desc(N, H, W, C, M, KH, KW, stride, pad, in_fmt, acc_fmt, out_fmt, act=ACT_NONE,
-              algo=ALGO_AUTO, round=ROUND_NEAREST_EVEN):
+              algo=ALGO_AUTO, round=ROUND_NEAREST_EVEN, ofm_kind=OFM_PLANES):
     return ConvDesc(N, H, W, C, M, KH, KW, stride, pad, fmt(in_fmt), fmt(acc_fmt), fmt(out_fmt),
-                    act, round, ORDER_KY_KX_C, algo)
+                    act, round, ORDER_KY_KX_C, algo, ofm_kind)
 
 
 def conv_out_hw(d):
@@ -153,11 +154,16 @@ def conv_out_hw(d):
 
 def conv2d(ifm, w, d, out=None):
     """ifm planes [N*H*W, ceil(C/32), NB_in], w planes [KH*KW*C, ceil(M/32), NB_in]
-    -> ofm planes [N*OH*OW, ceil(M/32), NB_out]."""
+    -> ofm planes [N*OH*OW, ceil(M/32), NB_out]; with d.ofm_kind OFM_F32 / OFM_CODE,
+    float32 values / int32 codes [N*OH*OW, M]."""
     OH, OW = conv_out_hw(d)
     if out is None:
-        out = torch.empty(plane_shape(d.N * OH * OW, d.M, d.out_fmt), dtype=torch.int32,
-                          device=ifm.device)
+        if d.ofm_kind == OFM_PLANES:
+            out = torch.empty(plane_shape(d.N * OH * OW, d.M, d.out_fmt), dtype=torch.int32,
+                              device=ifm.device)
+        else:
+            out = torch.empty((d.N * OH * OW, d.M), device=ifm.device,
+                              dtype=torch.float32 if d.ofm_kind == OFM_F32 else torch.int32)
     _check(lib().hobflops_conv2d(_ptr(ifm), _ptr(w), _ptr(out), ctypes.byref(d), _stream(ifm)))
     return out
 

@@ -65,7 +65,8 @@ def test_conv_rejects_bad_descriptors(hf, bad):
 
 
 def test_conv_rejects_round_order_and_algo(hf):
-    for field, value in (("round", 2), ("round", -1), ("order", 2), ("algo", 3), ("algo", -1)):
+    for field, value in (("round", 2), ("round", -1), ("order", 2), ("algo", 3), ("algo", -1),
+                         ("ofm_kind", 3), ("ofm_kind", -1)):
         d = desc(hf)
         setattr(d, field, value)
         assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -1, field

@@ -206,3 +206,40 @@ def test_resnet_conv_layer_sampled():
     want = orc.conv2d_points(qi, qw, pts, 1, 1, 5, 3, 4, 4)
     gotp = got[pts[:, 0], pts[:, 1], pts[:, 2], pts[:, 3]]
     assert np.array_equal(gotp, want)
+
+
+@pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
+@pytest.mark.parametrize("M", [64, 40, 37])
+def test_conv_fused_unpack(algo, M):
+    """The unpack fused into the epilogue (ofm_kind F32 / CODE) equals the
+    oracle's codes and their float32 values: full row, ragged last m-tile,
+    a row length that is not a multiple of four, and an output that is only
+    4-byte aligned."""
+    hf = need_gpu()
+    g = np.random.default_rng([12, M, algo])
+    N, H, W, C = 2, 7, 9, 37
+    ifm = I.inject_specials(g.uniform(-2, 2, (N, H, W, C)).astype(np.float32), g, 0.01)
+    w = I.inject_specials(g.uniform(-1, 1, (3, 3, C, M)).astype(np.float32), g, 0.005)
+    qi, qw = orc.quantize_f32(ifm, 5, 3), orc.quantize_f32(w, 5, 3)
+    want = orc.conv2d(qi, qw, 1, 1, 5, 3, 4, 5, 1).reshape(-1, M)
+    pi = hf.pack(dev(qi.astype(np.uint32).view(np.int32).reshape(-1, C)), (5, 3))
+    pw = hf.pack(dev(qw.astype(np.uint32).view(np.int32).reshape(-1, M)), (5, 3))
+    P = want.shape[0]
+    for kind in (hf.OFM_CODE, hf.OFM_F32):
+        for offset in (0, 1):
+            say(f"conv fused unpack M={M} algo={algo} kind={kind} offset={offset}")
+            d = hf.conv_desc(N, H, W, C, M, 3, 3, 1, 1, (5, 3), (5, 4), (5, 5), hf.ACT_RELU, algo,
+                             ofm_kind=kind)
+            dt = torch.float32 if kind == hf.OFM_F32 else torch.int32
+            buf = torch.full((P * M + 8,), -1, dtype=dt, device="cuda")
+            out = buf[offset:offset + P * M].view(P, M)
+            hf.conv2d(pi, pw, d, out=out)
+            torch.cuda.synchronize()
+            got = out.cpu().numpy()
+            if kind == hf.OFM_CODE:
+                assert np.array_equal(got.view(np.uint32).astype(np.uint64), want)
+            else:
+                assert np.array_equal(got.view(np.uint32), orc.decode_f32(want, 5, 5).view(np.uint32))
+            rest = buf.cpu().numpy()
+            assert np.all(rest[:offset].view(np.int32) == -1) if dt == torch.int32 else True
+            assert np.all(rest[offset + P * M:].view(np.uint32) == rest[-1:].view(np.uint32))
