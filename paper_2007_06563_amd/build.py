@@ -85,7 +85,7 @@ def netlist(kind, key, rnd, cache):
 
 # Product ring depth and load schedule of the split kernel's accumulator role
 # (see gen/asmgen.split_functions).
-SPLIT_SLOTS, SPLIT_SCHEDULE = 2, "batch"
+SPLIT_SLOTS, SPLIT_SCHEDULE, SPLIT_SYNC = 2, "batch", "pairs"
 
 
 def split_batch(naccp, slots=None):
@@ -98,7 +98,8 @@ def split_batch(naccp, slots=None):
 def split_asm(wE, wi, wa, rnd, cache):
     """The split kernel's assembly for one variant, or None when the two
     netlists do not fit the registers the asm blocks may use."""
-    key = f"split_e{wE}m{wi}_a{wa}{variants._sfx(rnd)}"
+    key = (f"split_e{wE}m{wi}_a{wa}{variants._sfx(rnd)}"
+           f"_s{SPLIT_SLOTS}_{SPLIT_SCHEDULE}_{SPLIT_SYNC}")
     if key not in cache:
         r = variants.RND_NAME[rnd]
         nin, nacc = nb(wE, wi), nb(wE, wa)
@@ -107,7 +108,7 @@ def split_asm(wE, wi, wa, rnd, cache):
         try:
             text, stats = asmgen.split_functions(acc_c, prod_c, nin, nacc,
                                                  split_batch(asmgen.pad4(nacc)),
-                                                 SPLIT_SLOTS, SPLIT_SCHEDULE)
+                                                 SPLIT_SLOTS, SPLIT_SCHEDULE, SPLIT_SYNC)
             cache[key] = {"text": text, "stats": stats}
         except regalloc.AllocError as e:
             cache[key] = {"text": None, "stats": {"unavailable": str(e)}}
@@ -139,6 +140,7 @@ def generate(verbose=True):
   static constexpr const int* kProdSlot = conv_{tag}::kProdSlot;
   static constexpr const int* kWSlot = conv_{tag}::kWSlot;
   static constexpr int kSlots = conv_{tag}::kSlots;
+  static constexpr bool kPairs = conv_{tag}::kPairs;
   static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[(NACC + 3) & ~3],
                                                     const lds_u32* e0, const lds_u32* e1,
                                                     const lds_u32* e2, int nb) {{

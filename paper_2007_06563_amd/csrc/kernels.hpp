@@ -108,6 +108,10 @@ __device__ __forceinline__ void store_ofm(const uint32_t (&out)[NOUT], uint32_t*
 
 constexpr int kConvBlock = 256;  // positions per workgroup: four wave64s
 
+// Bound of every flag wait in the split kernel (sleeps of 64 clocks): a
+// counter that never arrives ends the wait instead of the kernel hanging.
+constexpr uint32_t kSpinCap = 1u << 20;
+
 // Kernel shapes of the convolution (hobflops_conv_desc.algo).
 constexpr int kAlgoAuto = 0, kAlgoFused = 1, kAlgoSplit = 2;
 
@@ -297,8 +301,12 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   static_assert(S == 2 || S == 3, "ring of two or three batches");
   static_assert(K * NIN <= kConvBlock, "one weight word per multiplier thread");
   static_assert(S * K * 256 * NACCP * 4 <= 144 * 1024, "product ring exceeds the LDS budget");
+  static_assert(!V::kPairs || (S == 2 && K * NIN <= 64), "pairs: two slots, weights by one wave");
   __shared__ uint4 pring[S * K * 4 * 64 * kStride];  // [slot][k][wave][lane][kStride]
-  __shared__ uint4 wring[3 * K * NINP / 4];          // [slot][k][NINP words]
+  // weights: shared ring [slot][k][NINP words] (barrier), or one batch per
+  // multiplier wave [wave][k][NINP words] (pairs)
+  __shared__ uint4 wring[(V::kPairs ? 4 : 3) * K * NINP / 4];
+  __shared__ uint32_t flags[4][2];  // pairs: per wave pair, batches made / consumed
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const bool mul_role = wave >= 4;
@@ -322,8 +330,9 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
     return (lds_u32*)(pring + ((((size_t)(b % S) * K + k) * 4 + pw) * 64 + lane) * kStride);
   };
 
-  // ---- multiplier waves: weight staging (thread t of the 256 loads word t)
-  const int mt_tid = threadIdx.x - 4 * 64;
+  // ---- multiplier waves: weight staging (thread t of the 256 loads word t;
+  // with pairs, lane t of each multiplier wave, for that wave alone)
+  const int mt_tid = V::kPairs ? lane : threadIdx.x - 4 * 64;
   uint32_t wstage = 0;
   auto fetch_w = [&](int b) {  // HBM -> register, rows of batch b (clamped)
     if (mt_tid < K * NIN) {
@@ -335,7 +344,8 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   auto store_w = [&](int b) {
     if (mt_tid < K * NIN) {
       const int k = mt_tid / NIN, bb = mt_tid - (mt_tid / NIN) * NIN;
-      reinterpret_cast<uint32_t*>(wring)[((b % 3) * K + k) * NINP + V::kWSlot[bb]] = wstage;
+      const int slot = V::kPairs ? pw : b % 3;
+      reinterpret_cast<uint32_t*>(wring)[(slot * K + k) * NINP + V::kWSlot[bb]] = wstage;
     }
   };
 
@@ -369,7 +379,7 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   auto produce = [&](int b) {
     const int t0 = b * K;
     const int tk = min(K, T - t0);
-    const lds_u32* wr = (const lds_u32*)wring + (b % 3) * K * NINP;
+    const lds_u32* wr = (const lds_u32*)wring + (V::kPairs ? pw : b % 3) * K * NINP;
     if (c == nc) advance();
     if (tk == K && c + K <= nc) {  // whole batch inside one channel word
       V::product_batch(xw, c, wr, entry(b, 0));
@@ -414,6 +424,59 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   // accumulator wave on the same SIMD takes the issue slots it could have
   // filled once the data arrived; the accumulator keeps issuing nearly at its
   // single-wave rate either way.
+  if constexpr (V::kPairs) {
+    // Pairs: accumulator wave pw and multiplier wave 4+pw hand batches over
+    // through flags[pw] (made, consumed); LDS operations of one wave complete
+    // in order, so a counter written after a wave's stores (and a wait for
+    // them) shows those stores to a reader that reads the counter first. All
+    // waits are bounded by kSpinCap sleeps.
+    volatile uint32_t* made = &flags[pw][0];
+    volatile uint32_t* consumed = &flags[pw][1];
+    if (mul_role) {
+      *made = 0u;
+      *consumed = 0u;
+    }
+    __syncthreads();  // counters set before any wave reads them
+    if (mul_role) {
+      __builtin_amdgcn_s_setprio(3);
+      load_ifm(0, 0, 0);
+      // This lane's weight word of batches b, b+1, b+2 in three registers,
+      // each loaded three batches ahead of its use, so that a miss in this
+      // XCD's L2 is covered by three batches of work (the loop is unrolled by
+      // three so that no register still being loaded is copied).
+      uint32_t wa = 0, wb = 0, wc = 0;
+      fetch_w(0);
+      wa = wstage;
+      fetch_w(1);
+      wb = wstage;
+      fetch_w(2);
+      wc = wstage;
+      auto step = [&](int b, uint32_t& wreg) {
+        wstage = wreg;
+        store_w(b);  // this wave's weights of batch b (read back below, in order)
+        fetch_w(b + 3);
+        wreg = wstage;
+        if (b >= 2) {  // slot b % 2 held batch b-2: wait until it was added
+          for (uint32_t spin = 0; spin < kSpinCap; ++spin) {
+            if (__builtin_amdgcn_readfirstlane(*consumed) >= (uint32_t)(b - 1)) break;
+            __builtin_amdgcn_s_sleep(1);
+          }
+        }
+        produce(b);  // ends with its stores complete
+        *made = (uint32_t)(b + 1);
+      };
+      int b = 0;
+      for (; b + 3 <= nb; b += 3) {
+        step(b, wa);
+        step(b + 1, wb);
+        step(b + 2, wc);
+      }
+      if (b < nb) step(b, wa);
+      if (b + 1 < nb) step(b + 1, wb);
+      return;
+    }
+    V::accum_loop(acc, entry(0, 0), entry(1, 0), (const lds_u32*)&flags[pw][0], nb);
+  } else {
   if (mul_role) {
     __builtin_amdgcn_s_setprio(3);
     load_ifm(0, 0, 0);
@@ -434,6 +497,7 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
 #pragma unroll
   for (int j = 0; j < S; ++j) __syncthreads();
   V::accum_loop(acc, entry(0, 0), entry(1, 0), entry(S - 1, 0), nb);  // nb barriers
+  }
   if (!active) return;
   uint32_t planes[NACC], out[NOUT];
 #pragma unroll

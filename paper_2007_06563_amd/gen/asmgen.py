@@ -49,7 +49,10 @@ def _asm_string(lines):
     return "\n".join(f'      "{ln}\\n"' for ln in lines)
 
 
-def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch"):
+SPIN_CAP = 1 << 20  # bounded waits: a flag that never comes ends the wait after this many sleeps
+
+
+def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sync="barrier"):
     """C++ text (inside a variant's namespace) of the two asm functions and
     their slot tables, plus allocation statistics.
 
@@ -57,15 +60,28 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch"):
     slots-1 batches ahead). schedule: "batch" requests all K entries of a
     batch after its barrier; "step" requests entry k+1 before adding entry k;
     "prefetch" (slots 3) is "step" plus entry 0 of the next batch requested
-    before the last add of the current one."""
+    before the last add of the current one.
+
+    sync: "barrier" ends every batch with a workgroup barrier; "pairs" hands
+    batches over between one accumulator wave and its multiplier wave through
+    two LDS counters (at the flag address f: f+0 batches made, f+4 batches
+    consumed): before a batch the accumulator reads the counter together with
+    the batch's products and uses them if the counter shows the batch (LDS
+    operations of a wave complete in order, and the multiplier writes the
+    counter after its products); else it polls the counter alone, with a
+    sleep between reads, at most SPIN_CAP times, and reads the products again.
+    After the batch it writes the consumed count."""
     assert slots in (2, 3) and schedule in ("batch", "step", "prefetch")
     assert schedule != "prefetch" or slots == 3
+    assert sync in ("barrier", "pairs")
+    assert sync == "barrier" or (slots == 2 and schedule == "batch")
     ninp, naccp = pad4(nin), pad4(nacc)
     kstride = naccp // 4
     A = list(range(BASE, BASE + naccp))
     B = list(range(BASE + naccp, BASE + 2 * naccp))
     P = [list(range(BASE + (2 + k) * naccp, BASE + (3 + k) * naccp)) for k in range(K)]
-    pool = list(range(BASE + (2 + K) * naccp, TOP))
+    VF, VB = TOP - 1, TOP - 2  # flag value read, consumed count written ("pairs")
+    pool = list(range(BASE + (2 + K) * naccp, TOP - 2 if sync == "pairs" else TOP))
     lines, place, st_acc = allocate(accum_C, {"acc": Block(A), "p": Block(P[0])},
                                     {"acc": (Block(B), "acc")}, pool)
     acc_slot = [r - BASE for r in place["in"]["acc"]]
@@ -106,6 +122,83 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch"):
     # The wait before adding entry k leaves in flight only the loads issued
     # after entry k's (LDS operations complete in order). Loads still in
     # flight at a barrier are carried across it ("prefetch" only).
+    def pair_batch(slot):
+        """One batch handed over through the counters (see sync). The
+        counter is read together with the batch's products; if it does not
+        show the batch yet, the products are dropped and only the counter is
+        read again, after a sleep, until it does (at most SPIN_CAP times);
+        then the products are read once more."""
+        n_reads = K * kstride
+        out = [f"ds_read_b32 v{VF}, %[fl]"]
+        for k in range(K):
+            out += reads(slot, k)
+        # the counter is the oldest operation in flight: any count below the
+        # loads issued after it (the field holds at most 15) waits for it
+        out += [f"s_waitcnt lgkmcnt({min(n_reads, 15)})",
+                f"v_readfirstlane_b32 %[t], v{VF}",
+                "s_nop 4",
+                "s_cmp_ge_u32 %[t], %[b1]",
+                f"s_cbranch_scc1 L%=_go{slot}",
+                "s_waitcnt lgkmcnt(0)",             # batch not made yet: drop the loads
+                "s_mov_b32 %[spin], 0",
+                f"L%=_poll{slot}:",
+                "s_sleep 1",
+                f"ds_read_b32 v{VF}, %[fl]",
+                "s_waitcnt lgkmcnt(0)",
+                f"v_readfirstlane_b32 %[t], v{VF}",
+                "s_nop 4",
+                "s_add_u32 %[spin], %[spin], 1",
+                "s_cmp_ge_u32 %[t], %[b1]",
+                f"s_cbranch_scc1 L%=_again{slot}",
+                f"s_cmp_lt_u32 %[spin], {SPIN_CAP}",
+                f"s_cbranch_scc1 L%=_poll{slot}",
+                f"L%=_again{slot}:"]
+        for k in range(K):
+            out += reads(slot, k)
+        out += [f"L%=_go{slot}:"]
+        for k in range(K):
+            out.append(f"s_waitcnt lgkmcnt({(K - 1 - k) * kstride})")
+            out += netlist(k)
+        out += [f"v_mov_b32 v{VB}, %[b1]",
+                "s_nop 4",                         # VALU result -> LDS store data
+                f"ds_write_b32 %[fl], v{VB} offset:4",
+                "s_add_u32 %[b1], %[b1], 1"]
+        return out
+
+    if sync == "pairs":
+        body = ["s_waitcnt lgkmcnt(0)", "s_mov_b32 %[n], %[nb]", "s_mov_b32 %[b1], 1",
+                "L%=_loop:"]
+        for slot in range(2):
+            body += pair_batch(slot)
+            body += ["s_sub_u32 %[n], %[n], 1",
+                     "s_cmp_eq_u32 %[n], 0",
+                     "s_cbranch_scc1 L%=_done"]
+        body += ["s_branch L%=_loop", "L%=_done:", "s_waitcnt lgkmcnt(0)"]
+        used = set(B) | set(r for blk in P for r in blk) | set(st_acc["temps"]) | {VF, VB}
+        clob = ", ".join(f'"v{r}"' for r in sorted(used))
+        state = ", ".join(f'"+{{v{BASE + s}}}"(acc[{s}])' for s in range(naccp))
+        accum_fn = f"""static constexpr int kAccSlot[{nacc}] = {{{", ".join(map(str, acc_slot))}}};
+static constexpr int kProdSlot[{nacc}] = {{{", ".join(map(str, prod_slot))}}};
+static constexpr int kSlots = 2;
+static constexpr bool kPairs = true;
+// The accumulator role: nb batches of K products from the two-slot LDS ring
+// (this lane's first entry of slot s at e_s, batch b in slot b % 2), handed
+// over by the multiplier wave through the counters at fl (made at fl, consumed
+// at fl + 4); acc holds the planes in register-slot order.
+static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], const lds_u32* e0,
+                                                  const lds_u32* e1, const lds_u32* fl, int nb) {{
+  uint32_t n, b1, spin, t;
+  asm volatile(
+{_asm_string(body)}
+      : {state}, [n] "=&s"(n), [b1] "=&s"(b1), [spin] "=&s"(spin), [t] "=&s"(t)
+      : [e0] "v"(e0), [e1] "v"(e1), [fl] "v"(fl), [nb] "s"(nb)
+      : {clob}, "scc", "memory");
+}}
+"""
+        mul_fn, stats = _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot,
+                                       entry_bytes, st_acc)
+        return accum_fn + mul_fn, stats
+
     carried = [("r", 0, 0)] if schedule == "prefetch" else []
     body = ["s_waitcnt lgkmcnt(0)"]  # nothing of the compiler's in flight: counts below are exact
     if carried:
@@ -136,6 +229,7 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch"):
     accum_fn = f"""static constexpr int kAccSlot[{nacc}] = {{{", ".join(map(str, acc_slot))}}};
 static constexpr int kProdSlot[{nacc}] = {{{", ".join(map(str, prod_slot))}}};
 static constexpr int kSlots = {slots};
+static constexpr bool kPairs = false;
 // The accumulator role: nb batches of K products from the LDS ring of kSlots
 // slots (this lane's first entry of slot s at e_s, batch b in slot b % kSlots),
 // one barrier after each batch; acc holds the planes in register-slot order.
@@ -149,6 +243,13 @@ static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], cons
       : {clob}, "scc", "memory");
 }}
 """
+    mul_fn, stats = _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot,
+                                   entry_bytes, st_acc)
+    return accum_fn + mul_fn, stats
+
+
+def _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot, entry_bytes, st_acc):
+    """The multiplier role's asm functions (the same for both sync modes)."""
     # ---- multiplier role: product planes go to the P block in slot order
     # (plane b at word prod_slot[b]), so a product is stored with 16-byte
     # writes; the banks of the product planes are thereby fixed.
@@ -222,4 +323,4 @@ static __device__ __forceinline__ void product_step(const uint32_t (&xw)[{nin}],
 """
     stats = {"accum": {k: v for k, v in st_acc.items() if k != "temps"},
              "mul": {k: v for k, v in st_mul.items() if k != "temps"}}
-    return accum_fn + mul_fn, stats
+    return mul_fn, stats

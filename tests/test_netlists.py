@@ -219,17 +219,24 @@ def test_split_asm_allocation(wE, wi, wa):
                 assert np.array_equal(regs[r], w), (C.name, grp, r)
 
 
-def test_split_asm_text():
-    """Shape of the generated accumulator loop: one barrier per batch,
-    wait counts within the 4-bit field, registers within v96..v255."""
+@pytest.mark.parametrize("sync", ["barrier", "pairs"])
+@pytest.mark.parametrize("wE,wi,wa", [(5, 3, 4), (5, 4, 5)])
+def test_split_asm_text(wE, wi, wa, sync):
+    """Shape of the generated accumulator loop: one barrier per batch, or
+    (pairs) none but a bounded counter wait and a consumed-count store per
+    batch; wait counts within the 4-bit field; registers within v96..v255."""
     import re
-    wE, wi, wa = 5, 3, 4
     nin, nacc = nbits(wE, wi), nbits(wE, wa)
     acc_c = opt.optimize(fp.accumulate_circuit(wE, wa))
     prod_c = opt.optimize(fp.product_circuit(wE, wi, wa))
-    text, _ = asmgen.split_functions(acc_c, prod_c, nin, nacc, 4)
+    text, _ = asmgen.split_functions(acc_c, prod_c, nin, nacc, 4, sync=sync)
     loop = text[text.index("accum_loop("):text.index("kWSlot")]
-    assert loop.count("s_barrier") == 2
+    if sync == "barrier":
+        assert loop.count("s_barrier") == 2
+    else:
+        assert "s_barrier" not in loop
+        assert loop.count("s_sleep") == 2 and loop.count("v_readfirstlane_b32") == 4
+        assert loop.count("ds_write_b32") == 2 and f"{asmgen.SPIN_CAP}" in loop
     waits = [int(x) for x in re.findall(r"lgkmcnt\((\d+)\)", text)]
     assert waits and max(waits) <= 15
     regs = [int(x) for x in re.findall(r"\bv(\d+)\b", text)]
