@@ -143,8 +143,9 @@ def generate(verbose=True):
   static constexpr bool kPairs = conv_{tag}::kPairs;
   static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[(NACC + 3) & ~3],
                                                     const lds_u32* e0, const lds_u32* e1,
-                                                    const lds_u32* e2, int nb) {{
-    conv_{tag}::accum_loop(acc, e0, e1, e2, nb);
+                                                    const lds_u32* e2, const lds_u32* fl,
+                                                    int nb) {{
+    conv_{tag}::accum_loop(acc, e0, e1, e2, fl, nb);
   }}
   static __device__ __forceinline__ void product_step(const uint32_t (&xw)[NIN], int c,
                                                       const lds_u32* wrow, lds_u32* entry) {{

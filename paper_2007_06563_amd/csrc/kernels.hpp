@@ -301,7 +301,7 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   static_assert(S == 2 || S == 3, "ring of two or three batches");
   static_assert(K * NIN <= kConvBlock, "one weight word per multiplier thread");
   static_assert(S * K * 256 * NACCP * 4 <= 144 * 1024, "product ring exceeds the LDS budget");
-  static_assert(!V::kPairs || (S == 2 && K * NIN <= 64), "pairs: two slots, weights by one wave");
+  static_assert(!V::kPairs || K * NIN <= 64, "pairs: a batch's weights loaded by one wave");
   __shared__ uint4 pring[S * K * 4 * 64 * kStride];  // [slot][k][wave][lane][kStride]
   // weights: shared ring [slot][k][NINP words] (barrier), or one batch per
   // multiplier wave [wave][k][NINP words] (pairs)
@@ -333,24 +333,33 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   // ---- multiplier waves: weight staging (thread t of the 256 loads word t;
   // with pairs, lane t of each multiplier wave, for that wave alone)
   const int mt_tid = V::kPairs ? lane : threadIdx.x - 4 * 64;
+  const bool w_lane = mt_tid < K * NIN;  // this thread moves weight word (wk, wbb) of a batch
+  const int wk = w_lane ? mt_tid / NIN : 0, wbb = w_lane ? mt_tid - wk * NIN : 0;
+  // its LDS word within a weight slot, looked up once: a table read inside the
+  // loop would be a memory load, and the wait for it would also wait for the
+  // weight and IFM loads issued ahead
+  const int w_ofs = wk * NINP + V::kWSlot[wbb];
   uint32_t wstage = 0;
   auto fetch_w = [&](int b) {  // HBM -> register, rows of batch b (clamped)
-    if (mt_tid < K * NIN) {
-      const int k = mt_tid / NIN, bb = mt_tid - (mt_tid / NIN) * NIN;
-      const int t = min(b * K + k, T - 1);
-      wstage = wm[(size_t)t * wrow + bb];
-    }
+    // every lane loads (the others a word they do not store): a load under a
+    // branch leaves the compiler's wait for it conservative, waiting for all
+    wstage = wm[(size_t)min(b * K + wk, T - 1) * wrow + wbb];
   };
   auto store_w = [&](int b) {
-    if (mt_tid < K * NIN) {
-      const int k = mt_tid / NIN, bb = mt_tid - (mt_tid / NIN) * NIN;
+    if (w_lane) {
       const int slot = V::kPairs ? pw : b % 3;
-      reinterpret_cast<uint32_t*>(wring)[(slot * K + k) * NINP + V::kWSlot[bb]] = wstage;
+      ((lds_u32*)wring)[slot * K * NINP + w_ofs] = wstage;
     }
   };
 
-  // ---- multiplier waves: IFM words of the current and the next chunk
-  uint32_t xw[NIN], xn[NIN];
+  // ---- multiplier waves: IFM words of the current and the next chunk. The
+  // next chunk's words are loaded into 16-byte register quads, so that the
+  // loads land in the registers they are read from a chunk later (loaded into
+  // scattered registers, they would be copied, and the copy waits for them).
+  constexpr int NQ = (NIN + 3) / 4;
+  typedef uint32_t quad_t __attribute__((ext_vector_type(4)));  // stays one 4-register value
+  uint32_t xw[NIN];
+  quad_t xq[NQ];
   bool xn_valid = false;          // xn is a real tap (else the chunk reads as +0)
   int nky = 0, nkx = 0, ncg = 0;  // coordinates of the chunk held in xn
   int c = 0, nc = 0;              // channel within the current chunk, its size
@@ -360,11 +369,24 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
     const uint32_t* ip =
         img + (((size_t)(xn_valid ? iy : 0) * p.W + (xn_valid ? ix : 0)) * p.CG + cg) * NIN;
 #pragma unroll
-    for (int b = 0; b < NIN; ++b) xn[b] = ip[b];
+    for (int q = 0; q < NQ; ++q) {
+      quad_t v = {0u, 0u, 0u, 0u};
+      __builtin_memcpy(&v, ip + 4 * q, 4 * min(4, NIN - 4 * q));
+      xq[q] = v;
+    }
   };
   auto advance = [&]() {  // move to the next (ky, kx, channel-word) chunk
+    // the copies are ordered before the next chunk's loads (asm statements
+    // keep their order, and loads do not cross the memory clobber): were the
+    // loads scheduled first, the old and new words would need separate
+    // registers, and the compiler would copy the new ones, waiting for them
 #pragma unroll
-    for (int bb = 0; bb < NIN; ++bb) xw[bb] = xn_valid ? xn[bb] : 0u;
+    for (int bb = 0; bb < NIN; ++bb) {
+      uint32_t v;
+      asm volatile("v_mov_b32 %0, %1" : "=v"(v) : "v"(xq[bb / 4][bb % 4]));
+      xw[bb] = xn_valid ? v : 0u;
+    }
+    asm volatile("" ::: "memory");
     nc = min(32, p.C - 32 * ncg);
     c = 0;
     if (++ncg == p.CG) {
@@ -430,8 +452,10 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
     // in order, so a counter written after a wave's stores (and a wait for
     // them) shows those stores to a reader that reads the counter first. All
     // waits are bounded by kSpinCap sleeps.
-    volatile uint32_t* made = &flags[pw][0];
-    volatile uint32_t* consumed = &flags[pw][1];
+    // LDS pointers, so that the polls are LDS reads (a generic pointer makes
+    // them flat accesses, whose waits also wait for every global load in flight)
+    volatile lds_u32* made = (volatile lds_u32*)&flags[pw][0];
+    volatile lds_u32* consumed = (volatile lds_u32*)&flags[pw][1];
     if (mul_role) {
       *made = 0u;
       *consumed = 0u;
@@ -456,9 +480,9 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
         store_w(b);  // this wave's weights of batch b (read back below, in order)
         fetch_w(b + 3);
         wreg = wstage;
-        if (b >= 2) {  // slot b % 2 held batch b-2: wait until it was added
+        if (b >= S) {  // slot b % S held batch b-S: wait until it was added
           for (uint32_t spin = 0; spin < kSpinCap; ++spin) {
-            if (__builtin_amdgcn_readfirstlane(*consumed) >= (uint32_t)(b - 1)) break;
+            if (__builtin_amdgcn_readfirstlane(*consumed) >= (uint32_t)(b - S + 1)) break;
             __builtin_amdgcn_s_sleep(1);
           }
         }
@@ -475,7 +499,8 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
       if (b + 1 < nb) step(b + 1, wb);
       return;
     }
-    V::accum_loop(acc, entry(0, 0), entry(1, 0), (const lds_u32*)&flags[pw][0], nb);
+    V::accum_loop(acc, entry(0, 0), entry(1, 0), entry(S - 1, 0), (const lds_u32*)&flags[pw][0],
+                  nb);
   } else {
   if (mul_role) {
     __builtin_amdgcn_s_setprio(3);
@@ -496,7 +521,7 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   }
 #pragma unroll
   for (int j = 0; j < S; ++j) __syncthreads();
-  V::accum_loop(acc, entry(0, 0), entry(1, 0), entry(S - 1, 0), nb);  // nb barriers
+  V::accum_loop(acc, entry(0, 0), entry(1, 0), entry(S - 1, 0), nullptr, nb);  // nb barriers
   }
   if (!active) return;
   uint32_t planes[NACC], out[NOUT];

@@ -4,7 +4,7 @@ The two wave roles of the split kernel run their netlists as inline assembly
 with explicit registers chosen by gen.regalloc, so that no VALU instruction
 reads two VGPRs of one bank (see gen/regalloc.py). The functions produced:
 
-* ``accum_loop(acc, e0, e1, e2, nb)``: the whole accumulator role. Batch b
+* ``accum_loop(acc, e0, e1, e2, fl, nb)``: the whole accumulator role. Batch b
   (K products) sits in slot b % kSlots of the LDS product ring; its entries
   are requested with 16-byte loads at immediate offsets from this lane's first
   entry, on the schedule split_functions is given, and K copies of the adder
@@ -33,6 +33,13 @@ from .regalloc import Block, allocate
 
 BASE = 96
 TOP = 256
+
+
+# Every netlist instruction is an 8-byte VOP3 encoding. Measured on gfx950, a
+# run of them issues at 4.04 clocks per instruction when each starts on an
+# 8-byte boundary and at 5.04 when each straddles one, so every run starts
+# with an alignment directive (the assembler pads with a 4-byte s_nop 0).
+ALIGN8 = ".p2align 3"
 
 
 def pad4(n):
@@ -70,11 +77,16 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
     operations of a wave complete in order, and the multiplier writes the
     counter after its products); else it polls the counter alone, with a
     sleep between reads, at most SPIN_CAP times, and reads the products again.
-    After the batch it writes the consumed count."""
-    assert slots in (2, 3) and schedule in ("batch", "step", "prefetch")
+    After the batch it writes the consumed count. With schedule "early" the
+    consumed count is written as soon as the last entry's products are in
+    registers, and the counter and entry 0 of the next batch are requested
+    before that entry is added, so that the check at the top of the next
+    batch finds them arrived."""
+    assert slots in (2, 3) and schedule in ("batch", "step", "prefetch", "early")
     assert schedule != "prefetch" or slots == 3
     assert sync in ("barrier", "pairs")
-    assert sync == "barrier" or (slots == 2 and schedule == "batch")
+    assert sync == "barrier" or schedule in ("batch", "early")
+    assert sync == "pairs" or schedule != "early"
     ninp, naccp = pad4(nin), pad4(nacc)
     kstride = naccp // 4
     A = list(range(BASE, BASE + naccp))
@@ -93,12 +105,13 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
                 f"offset:{k * entry_bytes + 16 * j}" for j in range(kstride)]
 
     def netlist(k):
+        """Entry k's adder, 8-byte aligned (see ALIGN8)."""
         m = {}
         if k % 2 == 1:  # B -> A
             m.update({a: b for a, b in zip(A, B)})
             m.update({b: a for a, b in zip(A, B)})
         m.update({p0: pk for p0, pk in zip(P[0], P[k])})
-        return _rename(lines, m)
+        return [ALIGN8] + _rename(lines, m)
 
     # Events of one batch in issue order: ("r", slot, k) loads entry k of a
     # slot, ("n", k) adds entry k of the current slot.
@@ -129,12 +142,19 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
         read again, after a sleep, until it does (at most SPIN_CAP times);
         then the products are read once more."""
         n_reads = K * kstride
-        out = [f"ds_read_b32 v{VF}, %[fl]"]
-        for k in range(K):
-            out += reads(slot, k)
+        early = schedule == "early"
+        if early:
+            # the counter and entry 0 were requested during the previous batch
+            # (or before the loop); only entry 0's loads were issued after it
+            out, ctr_wait = [], kstride
+        else:
+            out = [f"ds_read_b32 v{VF}, %[fl]"]
+            for k in range(K):
+                out += reads(slot, k)
+            ctr_wait = min(n_reads, 15)
         # the counter is the oldest operation in flight: any count below the
         # loads issued after it (the field holds at most 15) waits for it
-        out += [f"s_waitcnt lgkmcnt({min(n_reads, 15)})",
+        out += [f"s_waitcnt lgkmcnt({ctr_wait})",
                 f"v_readfirstlane_b32 %[t], v{VF}",
                 "s_nop 4",
                 "s_cmp_ge_u32 %[t], %[b1]",
@@ -153,22 +173,36 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
                 f"s_cmp_lt_u32 %[spin], {SPIN_CAP}",
                 f"s_cbranch_scc1 L%=_poll{slot}",
                 f"L%=_again{slot}:"]
-        for k in range(K):
-            out += reads(slot, k)
-        out += [f"L%=_go{slot}:"]
+        release = [f"v_mov_b32 v{VB}, %[b1]",
+                   "s_nop 4",                      # VALU result -> LDS store data
+                   f"ds_write_b32 %[fl], v{VB} offset:4"]
+        if early:
+            out += reads(slot, 0) + [f"L%=_go{slot}:"]
+            for k in range(1, K):
+                out += reads(slot, k)
+        else:
+            for k in range(K):
+                out += reads(slot, k)
+            out += [f"L%=_go{slot}:"]
         for k in range(K):
             out.append(f"s_waitcnt lgkmcnt({(K - 1 - k) * kstride})")
+            if early and k == K - 1:
+                # every product of this batch is in registers: release the
+                # slot, then request the next batch's counter and entry 0
+                # (after the last batch they are read and never used)
+                out += release + [f"ds_read_b32 v{VF}, %[fl]"] + reads((slot + 1) % slots, 0)
             out += netlist(k)
-        out += [f"v_mov_b32 v{VB}, %[b1]",
-                "s_nop 4",                         # VALU result -> LDS store data
-                f"ds_write_b32 %[fl], v{VB} offset:4",
-                "s_add_u32 %[b1], %[b1], 1"]
+        if not early:
+            out += release
+        out += ["s_add_u32 %[b1], %[b1], 1"]
         return out
 
     if sync == "pairs":
-        body = ["s_waitcnt lgkmcnt(0)", "s_mov_b32 %[n], %[nb]", "s_mov_b32 %[b1], 1",
-                "L%=_loop:"]
-        for slot in range(2):
+        body = ["s_waitcnt lgkmcnt(0)", "s_mov_b32 %[n], %[nb]", "s_mov_b32 %[b1], 1"]
+        if schedule == "early":
+            body += [f"ds_read_b32 v{VF}, %[fl]"] + reads(0, 0)
+        body += ["L%=_loop:"]
+        for slot in range(slots):
             body += pair_batch(slot)
             body += ["s_sub_u32 %[n], %[n], 1",
                      "s_cmp_eq_u32 %[n], 0",
@@ -179,19 +213,20 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
         state = ", ".join(f'"+{{v{BASE + s}}}"(acc[{s}])' for s in range(naccp))
         accum_fn = f"""static constexpr int kAccSlot[{nacc}] = {{{", ".join(map(str, acc_slot))}}};
 static constexpr int kProdSlot[{nacc}] = {{{", ".join(map(str, prod_slot))}}};
-static constexpr int kSlots = 2;
+static constexpr int kSlots = {slots};
 static constexpr bool kPairs = true;
-// The accumulator role: nb batches of K products from the two-slot LDS ring
-// (this lane's first entry of slot s at e_s, batch b in slot b % 2), handed
-// over by the multiplier wave through the counters at fl (made at fl, consumed
-// at fl + 4); acc holds the planes in register-slot order.
+// The accumulator role: nb batches of K products from the LDS ring of kSlots
+// slots (this lane's first entry of slot s at e_s, batch b in slot b % kSlots),
+// handed over by the multiplier wave through the counters at fl (made at fl,
+// consumed at fl + 4); acc holds the planes in register-slot order.
 static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], const lds_u32* e0,
-                                                  const lds_u32* e1, const lds_u32* fl, int nb) {{
+                                                  const lds_u32* e1, const lds_u32* e2,
+                                                  const lds_u32* fl, int nb) {{
   uint32_t n, b1, spin, t;
   asm volatile(
 {_asm_string(body)}
       : {state}, [n] "=&s"(n), [b1] "=&s"(b1), [spin] "=&s"(spin), [t] "=&s"(t)
-      : [e0] "v"(e0), [e1] "v"(e1), [fl] "v"(fl), [nb] "s"(nb)
+      : [e0] "v"(e0), [e1] "v"(e1), [e2] "v"(e2), [fl] "v"(fl), [nb] "s"(nb)
       : {clob}, "scc", "memory");
 }}
 """
@@ -232,9 +267,11 @@ static constexpr int kSlots = {slots};
 static constexpr bool kPairs = false;
 // The accumulator role: nb batches of K products from the LDS ring of kSlots
 // slots (this lane's first entry of slot s at e_s, batch b in slot b % kSlots),
-// one barrier after each batch; acc holds the planes in register-slot order.
+// one barrier after each batch; acc holds the planes in register-slot order
+// (fl, the pairs' counters, is not used).
 static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], const lds_u32* e0,
-                                                  const lds_u32* e1, const lds_u32* e2, int nb) {{
+                                                  const lds_u32* e1, const lds_u32* e2,
+                                                  const lds_u32* fl, int nb) {{
   uint32_t n;
   asm volatile(
 {_asm_string(body)}
@@ -269,9 +306,9 @@ def _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot, entry_
         block k%2."""
         m = {w0: wk for w0, wk in zip(W[0], W[k])}
         m.update({p0: pj for p0, pj in zip(PB[0], PB[k % 2])})
-        out = [f"v_bfe_i32 v{r}, %[x{b}], {creg}, 1" for b, r in enumerate(xregs)]
+        out = [ALIGN8] + [f"v_bfe_i32 v{r}, %[x{b}], {creg}, 1" for b, r in enumerate(xregs)]
         out.append(f"s_waitcnt lgkmcnt({wait})")
-        out += _rename(plines, m)
+        out += [ALIGN8] + _rename(plines, m)
         out.append("s_nop 4")  # VALU results -> LDS store data
         for j in range(kstride):
             r0 = PB[k % 2][4 * j]
