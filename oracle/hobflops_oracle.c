@@ -551,3 +551,44 @@ int hfo_conv2d_points(const uint64_t* ifm, const uint64_t* w, const int64_t* pts
   }
   return run_conv(ifm, w, out, pts, npts, d, nthreads);
 }
+
+/* ------------------------------------------------------------------------ */
+/* Average pooling. */
+
+uint64_t hfo_recip(uint64_t n, int wE, int wF)
+{
+  fmt_t f = {wE, wF};
+  if (!fmt_ok(f) || n == 0 || n > ((uint64_t)1 << 32)) return HFO_BAD_FORMAT;
+  /* 1/n = (q + r/n) * 2^-k with q = floor(2^k / n) of at least wF+3 bits;
+   * a sticky bit below q (set when r != 0) keeps the rounding exact */
+  int ln = 0;
+  while (ln < 64 && (n >> ln) != 0) ln++;
+  int k = wF + 3 + ln;
+  uint64_t q = ((uint64_t)1 << k) / n, r = ((uint64_t)1 << k) % n;
+  big M;
+  big_set_shl(&M, (q << 1) | (r != 0), 0);
+  return round_value(f, 0, &M, -(int64_t)k - 1, HFO_RNE);
+}
+
+int hfo_avgpool(const uint64_t* in, uint64_t* out, int N, int H, int W, int C, int wE, int wF_in,
+                int wF_acc, int wF_out, int round)
+{
+  fmt_t fi = {wE, wF_in}, fa = {wE, wF_acc}, fo = {wE, wF_out};
+  if (!in || !out || N < 1 || H < 1 || W < 1 || C < 1 || !fmt_ok(fi) || !fmt_ok(fa) ||
+      !fmt_ok(fo) || wF_in > wF_acc || !mode_ok(round))
+    return -1;
+  uint64_t scale = hfo_recip((uint64_t)H * (uint64_t)W, wE, wF_acc);
+  for (int n = 0; n < N; n++) {
+    for (int c = 0; c < C; c++) {
+      uint64_t acc = make_zero(0, fa);
+      for (int y = 0; y < H; y++) {
+        for (int x = 0; x < W; x++) {
+          uint64_t v = in[(((size_t)n * H + y) * W + x) * C + c];
+          acc = hfo_add_rm(acc, hfo_convert_rm(v, wE, wF_in, wF_acc, round), wE, wF_acc, round);
+        }
+      }
+      out[(size_t)n * C + c] = hfo_mul_rm(acc, scale, wE, wF_acc, wF_out, round);
+    }
+  }
+  return 0;
+}

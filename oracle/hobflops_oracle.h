@@ -114,6 +114,23 @@ int hfo_conv2d_points(const uint64_t* ifm, const uint64_t* w, const int64_t* pts
 /* Number of threads hfo_conv2d would use for nthreads <= 0. */
 int hfo_default_threads(void);
 
+/* The code, in format (wE, wF), of 1/n for an integer n >= 1, rounded to
+ * nearest with ties to even (the scale factor of average pooling). Returns
+ * HFO_BAD_FORMAT for a bad format or n = 0. */
+uint64_t hfo_recip(uint64_t n, int wE, int wF);
+
+/* Global average pooling, the layer between the last convolution and the
+ * fully connected layer of MobileNets that the paper proposes to build in the
+ * HOBFLOPS format (Sec. 4, on where the format transformation happens).
+ * in: codes in in_fmt, [N][H][W][C]; out: codes in out_fmt, [N][C].
+ * For every (n, c): acc = +0 in acc_fmt; for y, then x:
+ *   acc = add(acc, widen(in[n][y][x][c]))       (widening to acc_fmt is exact)
+ * then out = mul(acc, s) rounded into out_fmt, with s = hfo_recip(H*W) in
+ * acc_fmt. The adds and the mul round in mode `round`.
+ * All formats share wE; wF_in <= wF_acc. Returns 0, or -1 on bad arguments. */
+int hfo_avgpool(const uint64_t* in, uint64_t* out, int N, int H, int W, int C, int wE, int wF_in,
+                int wF_acc, int wF_out, int round);
+
 #ifdef __cplusplus
 }
 #endif

@@ -41,11 +41,14 @@ def load(path):
     L.hfo_muladd_rm_array.argtypes = [u64p, u64p, u64p, sz, ci, ci, ci, ci, u64p]
     L.hfo_conv2d.argtypes = [u64p, u64p, u64p, ctypes.POINTER(ConvDesc), ci]
     L.hfo_conv2d_points.argtypes = [u64p, u64p, i64p, sz, u64p, ctypes.POINTER(ConvDesc), ci]
+    L.hfo_recip.argtypes = [ctypes.c_uint64, ci, ci]
+    L.hfo_recip.restype = ctypes.c_uint64
+    L.hfo_avgpool.argtypes = [u64p, u64p, ci, ci, ci, ci, ci, ci, ci, ci, ci]
     for name in ("hfo_quantize_f32_array", "hfo_decode_f32_array", "hfo_mul_array",
                  "hfo_add_array", "hfo_convert_array", "hfo_relu_array",
                  "hfo_muladd_array", "hfo_conv2d", "hfo_conv2d_points",
                  "hfo_mul_rm_array", "hfo_add_rm_array", "hfo_convert_rm_array",
-                 "hfo_muladd_rm_array",
+                 "hfo_muladd_rm_array", "hfo_avgpool",
                  "hfo_default_threads"):
         getattr(L, name).restype = ctypes.c_int
     return L
@@ -164,4 +167,22 @@ def conv2d_points(ifm, w, pts, stride, pad, wE, wF_in, wF_acc, wF_out, act=0, nt
     _check((L or lib()).hfo_conv2d_points(_p(ifm, ctypes.c_uint64), _p(w, ctypes.c_uint64),
                                    _p(pts, ctypes.c_int64), len(pts), _p(r, ctypes.c_uint64),
                                    ctypes.byref(d), nthreads))
+    return r
+
+
+def recip(n, wE, wF, L=None):
+    """The code of 1/n in (wE, wF), rounded to nearest even."""
+    r = (L or lib()).hfo_recip(int(n), wE, wF)
+    if r == 0xFFFFFFFFFFFFFFFF:
+        raise ValueError("oracle rejected the arguments (format or n out of range)")
+    return np.uint64(r)
+
+
+def avgpool(x, wE, wF_in, wF_acc, wF_out, L=None, rnd=RNE):
+    """Global average pooling: x [N,H,W,C] codes -> [N,C] codes (hfo_avgpool)."""
+    x = _u64(x)
+    N, H, W, C = x.shape
+    r = np.empty((N, C), np.uint64)
+    _check((L or lib()).hfo_avgpool(_p(x, ctypes.c_uint64), _p(r, ctypes.c_uint64), N, H, W, C,
+                                    wE, wF_in, wF_acc, wF_out, int(rnd)))
     return r

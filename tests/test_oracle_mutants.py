@@ -14,6 +14,7 @@ import bruteforce as bf
 import oracle as orc
 from oracle import build as obuild
 from test_oracle_conv import ref_conv
+from test_oracle_pool import nearest_rational
 
 SRC = open(obuild.SRC).read()
 
@@ -53,6 +54,16 @@ MUTANTS = {
     "padding_index": ("int ix = ox * d->stride + kx - d->pad;", "int ix = ox * d->stride + kx;"),
     "relu_after_convert": ("  if (d->act == 1) acc = hfo_relu(acc, d->wE, d->wF_acc);\n  return hfo_convert_rm(",
                            "  return hfo_convert_rm("),
+    "pool_columns_first": ("for (int y = 0; y < H; y++) {\n        for (int x = 0; x < W; x++) {",
+                           "for (int x = 0; x < W; x++) {\n        for (int y = 0; y < H; y++) {"),
+    "pool_starts_at_neg_zero": ("uint64_t acc = make_zero(0, fa);", "uint64_t acc = make_zero(1, fa);"),
+    "pool_ignores_mode": ("acc = hfo_add_rm(acc, hfo_convert_rm(v, wE, wF_in, wF_acc, round), wE, wF_acc, round);",
+                          "acc = hfo_add_rm(acc, hfo_convert_rm(v, wE, wF_in, wF_acc, round), wE, wF_acc, HFO_RNE);"),
+    "recip_truncated": ("return round_value(f, 0, &M, -(int64_t)k - 1, HFO_RNE);",
+                        "return round_value(f, 0, &M, -(int64_t)k - 1, HFO_RTZ);"),
+    "recip_no_sticky": ("big_set_shl(&M, (q << 1) | (r != 0), 0);", "big_set_shl(&M, q << 1, 0);"),
+    "pool_scale_missing": ("out[(size_t)n * C + c] = hfo_mul_rm(acc, scale, wE, wF_acc, wF_out, round);",
+                           "out[(size_t)n * C + c] = hfo_convert_rm(acc, wE, wF_acc, wF_out, round);"),
 }
 
 
@@ -88,6 +99,21 @@ def refs():
     r["mul_rtz"] = bf.mul(a, b, 5, 3, 4, mode="rtz")
     r["add_rtz"] = bf.add(a2, b2, 4, 3, mode="rtz")
     r["conv_rtz"] = ref_conv(ifm, w, 1, 1, 5, 3, 4, 3, mode="rtz")
+    # pooling: the nearest codes of 1/n, and a 4 x 4 map whose mean depends on
+    # the summation order (see test_oracle_pool)
+    from fractions import Fraction
+    r["recip"] = [(n, nearest_rational(Fraction(1, n), 5, 10)) for n in range(1, 200)]
+    maps = np.ones((3, 4, 4, 1), np.float32)
+    maps[0, 3, 3, 0] = maps[1, 0, 0, 0] = maps[2, 0, 3, 0] = 64.0
+    r["pool_order"] = (bf.quantize(maps, 5, 3), bf.quantize(np.array([[5.0], [4.0], [4.0]], np.float32), 5, 3))
+    r["pool_zero"] = (bf.quantize(np.full((1, 2, 2, 1), -0.0, np.float32), 5, 4), np.zeros((1, 1), np.uint64))
+    pos = np.abs(g.normal(size=(1, 7, 7, 16))).astype(np.float32) + 0.01
+    xp = bf.quantize(pos, 5, 4)
+    scale = np.full(16, nearest_rational(Fraction(1, 49), 5, 4), np.uint64)
+    acc = np.zeros(16, np.uint64)
+    for i in range(49):               # rows, then columns; truncating adds
+        acc = bf.add(acc, xp.reshape(49, 16)[i], 5, 4, mode="rtz")
+    r["pool_rtz"] = (xp, bf.mul(acc, scale, 5, 4, 4, mode="rtz").reshape(1, 16))
     return r
 
 
@@ -120,6 +146,17 @@ def failures(L, r):
         bad.append("add_rtz")
     if not np.array_equal(orc.conv2d(ifm, w, 1, 1, 5, 3, 4, 3, L=L, rnd=orc.RTZ), r["conv_rtz"]):
         bad.append("conv_rtz")
+    if any(int(orc.recip(n, 5, 10, L=L)) != want for n, want in r["recip"]):
+        bad.append("recip")
+    maps, want = r["pool_order"]
+    if not np.array_equal(orc.avgpool(maps, 5, 3, 3, 3, L=L), want):
+        bad.append("pool_order")
+    zeros, want = r["pool_zero"]
+    if not np.array_equal(orc.avgpool(zeros, 5, 4, 4, 4, L=L), want):
+        bad.append("pool_zero")
+    x, want = r["pool_rtz"]
+    if not np.array_equal(orc.avgpool(x, 5, 4, 4, 4, L=L, rnd=orc.RTZ), want):
+        bad.append("pool_rtz")
     return bad
 
 
