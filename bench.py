@@ -40,6 +40,9 @@ PEAK_LANE_OPS = N_CU * LANES_PER_CU_CLK * CLOCK_HZ   # 7.86e13 32-bit VALU ops/s
 N_SIMD = N_CU * 4
 SINGLE_WAVE_SHARE = 0.5
 HBM_PEAK = 8.0e12
+# clocks per instruction of one wave running a netlist alone (measured on
+# MI355X over long 8-byte-aligned straight-line runs)
+ISSUE_CLOCKS = 4.04
 
 IN_FMT, ACC_FMT, OUT_FMT = (5, 3), (5, 4), (5, 4)
 
@@ -213,6 +216,28 @@ def suite(reps):
         "roofline": {"bound": "alu", "achieved": total_ops / (ms * 1e-3) / 1e12,
                      "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
                      "frac": total_ops / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
+    # global average pooling in the packed format: the stack's last 7 x 7 x 512
+    # map, and the MobileNets interface shape 7 x 7 x 1024, both batch 16
+    s_last = shapes[-1]
+    x1024 = hf.pack(torch.from_numpy(np.random.default_rng(5).normal(
+        size=(16 * 49, 1024)).astype(np.float32)).to(dev), (5, 4))
+    for name, src, C in (("13-layer stack output", acts[-1], s_last.M),
+                         ("MobileNets interface", x1024, 1024)):
+        N, H, W = 16, 7, 7
+        f = (5, 4)
+        o = hf.avgpool(src, N, H, W, C, f, f, f)
+        ms = _time(lambda: hf.avgpool(src, N, H, W, C, f, f, f, out=o), reps, stream)
+        ops = hf.avgpool_netlist_ops(f, f, f)
+        words = N * ((C + 31) // 32)
+        lane_ops = words * (H * W * ops["accum"] + ops["scale"])
+        chain_us = H * W * ops["accum"] * ISSUE_CLOCKS / 2.3e3
+        print(json.dumps({
+            "workload": f"global average pooling, {name}: {N}x{H}x{W}x{C}, (5,4)",
+            "kernel": "avgpool_kernel", "ms": ms, "g_adds": N * C * H * W / (ms * 1e-3) / 1e9,
+            "chain_bound_us": chain_us, "lanes": words,
+            "roofline": {"bound": "alu", "achieved": lane_ops / (ms * 1e-3) / 1e12,
+                         "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
+                         "frac": lane_ops / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
 
 
 def sweep(reps):

@@ -152,6 +152,33 @@ int hobflops_muladd_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int rou
 int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int round, int* conv_mac_ops,
                          int* conv_mul_ops, int* conv_accum_ops, int* muladd_ops);
 
+/* Global average pooling on PL32 planes: the pooling layer the paper proposes
+ * to build in the packed format, between MobileNets' last convolution and its
+ * fully connected layer (Sec. 4, on where the format transformation happens).
+ *   in:  [N * H * W][ceil(C/32)][NB_in]  (the planes of an NHWC tensor, as a
+ *        convolution writes them; padding channels hold +0)
+ *   out: [N][ceil(C/32)][NB_out]          (device memory owned by the caller)
+ * For each (n, c): acc = +0 in acc_fmt; for y, then x:
+ *   acc = add(acc, widen(in[n][y][x][c]))  (widening to acc_fmt is exact)
+ * then out = mul(acc, s) rounded into out_fmt, s the code of 1/(H*W) in
+ * acc_fmt rounded to nearest even (+0 if below the format's range). The adds
+ * and the multiply round in mode round (HOBFLOPS_ROUND_*). All formats share
+ * wE; acc_fmt.wF >= in_fmt.wF. in and out must not overlap.
+ * Returns HOBFLOPS_EINVAL (shape, format, null pointer), HOBFLOPS_EALIGN,
+ * HOBFLOPS_EUNSUPPORTED (combination not generated) or HOBFLOPS_EHIP. */
+int hobflops_avgpool(const uint32_t* in, uint32_t* out, int N, int H, int W, int C,
+                     hobflops_fmt in_fmt, hobflops_fmt acc_fmt, hobflops_fmt out_fmt, int round,
+                     void* stream);
+
+/* 1 if hobflops_avgpool has a kernel for these formats and rounding mode. */
+int hobflops_avgpool_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, hobflops_fmt out_fmt,
+                               int round);
+
+/* Bitwise VALU instructions per 32-lane word of the pooling netlists: one
+ * accumulating add and the final multiply. Any output pointer may be NULL. */
+int hobflops_avgpool_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, hobflops_fmt out_fmt,
+                                 int round, int* accum_ops, int* scale_ops);
+
 /* Text for a status code; for HOBFLOPS_EHIP, the last HIP error of this
  * thread. The pointer stays valid until the next call on the same thread. */
 const char* hobflops_status_string(int status);

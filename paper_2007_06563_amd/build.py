@@ -46,7 +46,7 @@ def netlist(kind, key, rnd, cache):
     """Optimised circuit for one operator (rounding mode rnd: variants.RNE or
     RTZ); cached per generator version."""
     name = {"mac": "mac_e{}m{}_a{}", "epi": "epi_e{}m{}_o{}{}", "muladd": "muladd_e{}m{}_a{}",
-            "prod": "prod_e{}m{}_a{}", "accum": "accum_e{}m{}"}[kind]
+            "prod": "prod_e{}m{}_a{}", "accum": "accum_e{}m{}", "scale": "scale_e{}m{}_o{}"}[kind]
     r = variants.RND_NAME[rnd]
     sfx = variants._sfx(rnd)
     if kind == "epi":
@@ -71,6 +71,9 @@ def netlist(kind, key, rnd, cache):
     elif kind == "epi":
         wE, wa, wo, act = key
         C = fp.convert_circuit(wE, wa, wo, relu=bool(act), canonical=True, rnd=r)
+        text_kw = {}
+    elif kind == "scale":
+        C = fp.mul_circuit(*key, canonical=True, rnd=r)
         text_kw = {}
     else:
         C = fp.muladd_circuit(*key, rnd=r)
@@ -224,6 +227,41 @@ hipError_t launch_muladd_{tag}(const uint32_t* a, const uint32_t* b, const uint3
 """
         files.append((f"muladd_{tag}.hip", src))
         reg_mul.append((v, tag, e["ops"]))
+    reg_pool = []
+    for v in variants.POOL_VARIANTS:
+        wE, wi, wa, wo, rnd = v
+        tag = variants.pool_tag(v)
+        accum, accum_e = netlist("accum", (wE, wa), rnd, cache)
+        scale, scale_e = netlist("scale", (wE, wa, wo), rnd, cache)
+        src = f"""// Generated: global average pooling variant {tag}. Do not edit.
+#include "kernels.hpp"
+#include "registry.hpp"
+namespace hobflops {{
+namespace pool_{tag} {{
+{cache[accum]['text']}
+{cache[scale]['text']}
+struct V {{
+  static constexpr int NIN = {nb(wE, wi)}, NACC = {nb(wE, wa)}, NOUT = {nb(wE, wo)};
+  static __device__ __forceinline__ void add(uint32_t (&acc)[NACC], const uint32_t (&x)[NACC]) {{
+    {accum}(acc, x);
+  }}
+  static __device__ __forceinline__ void scale(const uint32_t (&acc)[NACC], const uint32_t (&s)[NACC],
+                                               uint32_t (&out)[NOUT]) {{
+    {scale}(acc, s, out);
+  }}
+}};
+}}  // namespace pool_{tag}
+hipError_t launch_pool_{tag}(const uint32_t* in, uint32_t* out, const PoolParams& p,
+                              hipStream_t stream) {{
+  const int64_t lanes = (int64_t)p.N * p.CG;
+  hipLaunchKernelGGL(avgpool_kernel<pool_{tag}::V>, dim3((unsigned)((lanes + 255) / 256)), dim3(256),
+                     0, stream, in, out, p);
+  return hipGetLastError();
+}}
+}}  // namespace hobflops
+"""
+        files.append((f"pool_{tag}.hip", src))
+        reg_pool.append((v, tag, accum_e["ops"], scale_e["ops"]))
     reg = ["// Generated: table of kernel variants (host code). Do not edit.",
            '#include "registry.hpp"', "#ifndef __HIP_DEVICE_COMPILE__", "namespace hobflops {"]
     for v, tag, *_ in reg_conv:
@@ -232,6 +270,9 @@ hipError_t launch_muladd_{tag}(const uint32_t* a, const uint32_t* b, const uint3
     for v, tag, ops in reg_mul:
         reg.append(f"hipError_t launch_muladd_{tag}(const uint32_t*, const uint32_t*, const uint32_t*, "
                    f"uint32_t*, int64_t, hipStream_t);")
+    for v, tag, *_ in reg_pool:
+        reg.append(f"hipError_t launch_pool_{tag}(const uint32_t*, uint32_t*, const PoolParams&, "
+                   f"hipStream_t);")
     reg.append("const ConvVariant kConvVariants[] = {")
     for v, tag, ops, pops, aops, has_split in reg_conv:
         reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {v[4]}, {v[5]}, {has_split}, {ops}, "
@@ -243,6 +284,11 @@ hipError_t launch_muladd_{tag}(const uint32_t* a, const uint32_t* b, const uint3
         reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {ops}, launch_muladd_{tag}}},")
     reg.append("};")
     reg.append(f"const int kNumMuladdVariants = {len(reg_mul)};")
+    reg.append("const PoolVariant kPoolVariants[] = {")
+    for v, tag, aops, sops in reg_pool:
+        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {v[4]}, {aops}, {sops}, launch_pool_{tag}}},")
+    reg.append("};")
+    reg.append(f"const int kNumPoolVariants = {len(reg_pool)};")
     reg.append("}  // namespace hobflops")
     reg.append("#endif")
     files.append(("registry.hip", "\n".join(reg) + "\n"))

@@ -1,6 +1,7 @@
 // C ABI of libhobflops.so (declared in include/hobflops.h): argument checks,
 // variant dispatch and launches. Nothing here computes on the host.
 #include <hip/hip_runtime.h>
+#include <limits.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <string.h>
@@ -44,6 +45,47 @@ const MuladdVariant* find_muladd(hobflops_fmt in, hobflops_fmt acc, int round) {
       return &v;
   }
   return nullptr;
+}
+
+const PoolVariant* find_pool(hobflops_fmt in, hobflops_fmt acc, hobflops_fmt out, int round) {
+  if (acc.wE != in.wE || out.wE != in.wE) return nullptr;
+  for (int i = 0; i < kNumPoolVariants; ++i) {
+    const PoolVariant& v = kPoolVariants[i];
+    if (v.wE == in.wE && v.wF_in == in.wF && v.wF_acc == acc.wF && v.wF_out == out.wF &&
+        v.round == round)
+      return &v;
+  }
+  return nullptr;
+}
+
+// The code of 1/n (n >= 1) in format f, to nearest with ties to even. With
+// 2^(t-1) <= n < 2^t: a power of two is exact; otherwise 1/n = (2^t/n) 2^-t
+// with 2^t/n in (1, 2), whose fraction bits are floor(2^(t+wF)/n) - 2^wF,
+// rounded by the remainder. Below the smallest normal the code is +0.
+uint32_t recip_code(uint64_t n, hobflops_fmt f) {
+  int t = 0;
+  while (t < 64 && (n >> t) != 0) ++t;
+  const int64_t bias = ((int64_t)1 << (f.wE - 1)) - 1;
+  int64_t u;
+  uint64_t frac;
+  if ((n & (n - 1)) == 0) {
+    u = -(int64_t)(t - 1);
+    frac = 0;
+  } else {
+    u = -(int64_t)t;
+    const uint64_t num = (uint64_t)1 << (t + f.wF);
+    uint64_t q = num / n;
+    const uint64_t r = num % n;
+    if (2 * r > n || (2 * r == n && (q & 1u))) ++q;
+    if (q == ((uint64_t)1 << (f.wF + 1))) {  // rounded up into the next binade
+      q >>= 1;
+      ++u;
+    }
+    frac = q - ((uint64_t)1 << f.wF);
+  }
+  const int64_t eb = u + bias;
+  if (eb < 0) return 0u;
+  return (1u << (f.wF + f.wE + 1)) | ((uint32_t)eb << f.wF) | (uint32_t)frac;
 }
 
 int round_ok(int round) {
@@ -178,6 +220,42 @@ int hobflops_muladd(const uint32_t* a, const uint32_t* b, const uint32_t* c, uin
   if (!a || !b || !c || !r) return HOBFLOPS_EINVAL;
   if (!aligned(a) || !aligned(b) || !aligned(c) || !aligned(r)) return HOBFLOPS_EALIGN;
   return hip_status(v->launch(a, b, c, r, (n + 31) / 32, (hipStream_t)stream));
+}
+
+int hobflops_avgpool_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, hobflops_fmt out_fmt,
+                               int round) {
+  return fmt_ok(in_fmt) && fmt_ok(acc_fmt) && fmt_ok(out_fmt) && round_ok(round) &&
+         find_pool(in_fmt, acc_fmt, out_fmt, round) != nullptr;
+}
+
+int hobflops_avgpool(const uint32_t* in, uint32_t* out, int N, int H, int W, int C,
+                     hobflops_fmt in_fmt, hobflops_fmt acc_fmt, hobflops_fmt out_fmt, int round,
+                     void* stream) {
+  if (N < 1 || H < 1 || W < 1 || C < 1 || (int64_t)H * W > INT32_MAX) return HOBFLOPS_EINVAL;
+  if (!fmt_ok(in_fmt) || !fmt_ok(acc_fmt) || !fmt_ok(out_fmt) || !round_ok(round))
+    return HOBFLOPS_EINVAL;
+  if (acc_fmt.wE != in_fmt.wE || out_fmt.wE != in_fmt.wE || acc_fmt.wF < in_fmt.wF)
+    return HOBFLOPS_EINVAL;
+  const PoolVariant* v = find_pool(in_fmt, acc_fmt, out_fmt, round);
+  if (!v) return HOBFLOPS_EUNSUPPORTED;
+  if (!in || !out) return HOBFLOPS_EINVAL;
+  if (!aligned(in) || !aligned(out)) return HOBFLOPS_EALIGN;
+  PoolParams p;
+  p.N = N;
+  p.HW = H * W;
+  p.CG = (C + 31) / 32;
+  p.scale = recip_code((uint64_t)H * (uint64_t)W, acc_fmt);
+  return hip_status(v->launch(in, out, p, (hipStream_t)stream));
+}
+
+int hobflops_avgpool_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, hobflops_fmt out_fmt,
+                                 int round, int* accum_ops, int* scale_ops) {
+  if (!round_ok(round)) return HOBFLOPS_EINVAL;
+  const PoolVariant* v = find_pool(in_fmt, acc_fmt, out_fmt, round);
+  if (!v) return HOBFLOPS_EUNSUPPORTED;
+  if (accum_ops) *accum_ops = v->accum_ops;
+  if (scale_ops) *scale_ops = v->scale_ops;
+  return HOBFLOPS_OK;
 }
 
 int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int round,

@@ -36,6 +36,13 @@ struct ConvParams {
   int ofm_vec;   // ofm is 16-byte aligned (value rows may be stored 16 bytes at a time)
 };
 
+// Global average pooling: N images, HW positions each, CG channel words per
+// position; `scale` is the code of 1/HW in the accumulator format.
+struct PoolParams {
+  int N, HW, CG;
+  uint32_t scale;
+};
+
 // What the convolution writes (hobflops_conv_desc.ofm_kind): PL32 planes, or
 // per value, row-major [P][M], float32 values or uint32 codes.
 constexpr int kOfmPlanes = 0, kOfmF32 = 1, kOfmCode = 2;
@@ -551,6 +558,56 @@ __global__ __launch_bounds__(256) void muladd_kernel(const uint32_t* __restrict_
   V::muladd(av, bv, cv, rv);
 #pragma unroll
   for (int i = 0; i < NACC; ++i) r[g * NACC + i] = rv[i];
+}
+
+// Global average pooling on PL32 planes (the pooling layer the paper proposes
+// for MobileNets' interface between its last convolution and the fully
+// connected layer, Sec. 4). One lane is one (image n, channel word cg): 32
+// channels, one per bit. acc = +0; for each position i (rows, then columns):
+// acc = add(acc, widen(x_i)); then out = scale(acc, s) (a multiply by the code
+// of 1/HW, broadcast into planes). in: [N * HW][CG][NIN], out: [N][CG][NOUT].
+template <class V>
+__global__ __launch_bounds__(256) void avgpool_kernel(const uint32_t* __restrict__ in,
+                                                      uint32_t* __restrict__ out, PoolParams p) {
+  constexpr int NIN = V::NIN, NACC = V::NACC, NOUT = V::NOUT, DF = NACC - NIN;
+  typedef uint32_t quad_t __attribute__((ext_vector_type(4)));
+  constexpr int NQ = (NIN + 3) / 4;
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= (int64_t)p.N * p.CG) return;
+  const int64_t n = g / p.CG, cg = g - n * p.CG;
+  const uint32_t* src = in + ((size_t)n * p.HW * p.CG + cg) * NIN;
+  const size_t step = (size_t)p.CG * NIN;
+  auto load = [&](quad_t (&q)[NQ], const uint32_t* ptr) {  // NIN words into 4-word vectors
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) {
+      quad_t v = {0u, 0u, 0u, 0u};
+      __builtin_memcpy(&v, ptr + 4 * j, 4 * (NIN - 4 * j < 4 ? NIN - 4 * j : 4));
+      q[j] = v;
+    }
+  };
+  uint32_t acc[NACC];
+#pragma unroll
+  for (int b = 0; b < NACC; ++b) acc[b] = 0u;  // +0
+  quad_t cur[NQ], nxt[NQ];
+  load(cur, src);
+  for (int i = 0; i < p.HW; ++i) {
+    // the next position's words are requested before this one is added
+    if (i + 1 < p.HW) load(nxt, src + (size_t)(i + 1) * step);
+    uint32_t x[NACC];  // widened: fraction planes move up by DF, zeros below
+#pragma unroll
+    for (int b = 0; b < DF; ++b) x[b] = 0u;
+#pragma unroll
+    for (int b = 0; b < NIN; ++b) x[DF + b] = cur[b / 4][b % 4];
+    V::add(acc, x);
+#pragma unroll
+    for (int j = 0; j < NQ; ++j) cur[j] = nxt[j];
+  }
+  uint32_t sp[NACC], r[NOUT];
+#pragma unroll
+  for (int b = 0; b < NACC; ++b) sp[b] = ((p.scale >> b) & 1u) ? 0xFFFFFFFFu : 0u;
+  V::scale(acc, sp, r);
+#pragma unroll
+  for (int b = 0; b < NOUT; ++b) out[(size_t)g * NOUT + b] = r[b];
 }
 
 }  // namespace hobflops

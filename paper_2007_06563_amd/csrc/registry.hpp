@@ -30,9 +30,22 @@ struct MuladdVariant {
   muladd_launch_fn launch;
 };
 
+typedef hipError_t (*pool_launch_fn)(const uint32_t* in, uint32_t* out, const PoolParams& p,
+                                     hipStream_t stream);
+
+struct PoolVariant {
+  int wE, wF_in, wF_acc, wF_out;
+  int round;       // HOBFLOPS_ROUND_*
+  int accum_ops;   // VALU bitwise instructions of one accumulating add
+  int scale_ops;   // ... of the final multiply by the scale
+  pool_launch_fn launch;
+};
+
 extern const ConvVariant kConvVariants[];
 extern const int kNumConvVariants;
 extern const MuladdVariant kMuladdVariants[];
 extern const int kNumMuladdVariants;
+extern const PoolVariant kPoolVariants[];
+extern const int kNumPoolVariants;
 
 }  // namespace hobflops

@@ -45,7 +45,8 @@ class ConvDesc(ctypes.Structure):
 
 EXPORTS = ("hobflops_plane_words", "hobflops_pack", "hobflops_unpack", "hobflops_conv2d",
            "hobflops_conv2d_supported", "hobflops_muladd", "hobflops_muladd_supported",
-           "hobflops_netlist_ops", "hobflops_status_string")
+           "hobflops_netlist_ops", "hobflops_avgpool", "hobflops_avgpool_supported",
+           "hobflops_avgpool_netlist_ops", "hobflops_status_string")
 
 
 def lib():
@@ -65,6 +66,9 @@ def lib():
         L.hobflops_muladd.argtypes = [vp, vp, vp, vp, i64, Fmt, Fmt, ci, vp]
         L.hobflops_muladd_supported.argtypes = [Fmt, Fmt, ci]
         L.hobflops_netlist_ops.argtypes = [Fmt, Fmt, ci] + [ctypes.POINTER(ci)] * 4
+        L.hobflops_avgpool.argtypes = [vp, vp, ci, ci, ci, ci, Fmt, Fmt, Fmt, ci, vp]
+        L.hobflops_avgpool_supported.argtypes = [Fmt, Fmt, Fmt, ci]
+        L.hobflops_avgpool_netlist_ops.argtypes = [Fmt, Fmt, Fmt, ci] + [ctypes.POINTER(ci)] * 2
         L.hobflops_status_string.argtypes = [ci]
         L.hobflops_status_string.restype = ctypes.c_char_p
         for name in EXPORTS[:-1]:
@@ -195,3 +199,27 @@ def netlist_ops(in_fmt, acc_fmt, round=ROUND_NEAREST_EVEN):
     if rc != 0:
         raise HobflopsError(rc, lib().hobflops_status_string(rc).decode())
     return dict(zip(("mac", "mul", "accum", "muladd"), (x.value for x in v)))
+
+
+def avgpool(planes, N, H, W, C, in_fmt, acc_fmt, out_fmt, out=None, round=ROUND_NEAREST_EVEN):
+    """Global average pooling: planes [N*H*W, ceil(C/32), NB_in] -> [N, ceil(C/32), NB_out]."""
+    in_fmt, acc_fmt, out_fmt = fmt(in_fmt), fmt(acc_fmt), fmt(out_fmt)
+    if out is None:
+        out = torch.empty(plane_shape(N, C, out_fmt), dtype=torch.int32, device=planes.device)
+    _check(lib().hobflops_avgpool(_ptr(planes), _ptr(out), N, H, W, C, in_fmt, acc_fmt, out_fmt,
+                                  round, _stream(planes)))
+    return out
+
+
+def avgpool_supported(in_fmt, acc_fmt, out_fmt, round=ROUND_NEAREST_EVEN):
+    return bool(lib().hobflops_avgpool_supported(fmt(in_fmt), fmt(acc_fmt), fmt(out_fmt), round))
+
+
+def avgpool_netlist_ops(in_fmt, acc_fmt, out_fmt, round=ROUND_NEAREST_EVEN):
+    """dict of VALU ops per 32-lane word of the pooling netlists: 'accum', 'scale'."""
+    v = [ctypes.c_int() for _ in range(2)]
+    rc = lib().hobflops_avgpool_netlist_ops(fmt(in_fmt), fmt(acc_fmt), fmt(out_fmt), round,
+                                            *[ctypes.byref(x) for x in v])
+    if rc != 0:
+        raise HobflopsError(rc, lib().hobflops_status_string(rc).decode())
+    return dict(zip(("accum", "scale"), (x.value for x in v)))

@@ -9,6 +9,9 @@ Convolution variants are (wE, wF_in, wF_acc, wF_out, act, round):
   * the ReLU + format-change epilogues of a stack of layers whose inputs
     alternate between (5,3) and (5,5).
 Element-wise MAC variants are (wE, wF_in, wF_acc, round).
+Global average pooling variants are (wE, wF_in, wF_acc, wF_out, round): the
+output format of every "single" convolution variant of the sweep pooled in
+that format, and (5,4) pooled with one more fraction bit in the sum.
 """
 RNE, RTZ = 0, 1
 
@@ -22,6 +25,11 @@ CONV_VARIANTS = (
 
 MULADD_VARIANTS = [(wE, wi, wa, r) for r in (RNE, RTZ) for wE, wi, wa in
                    [(4, 2, 3), (5, 3, 4), (5, 5, 6), (5, 7, 8), (5, 10, 11), (8, 7, 8)]]
+
+POOL_VARIANTS = (
+    [(wE, m + 1, m + 1, m + 1, r) for r in (RNE, RTZ) for wE, m in SWEEP_TYPES]
+    + [(5, 4, 5, 4, RNE), (5, 4, 5, 4, RTZ)]
+)
 
 RND_NAME = {RNE: "rne", RTZ: "rtz"}
 
@@ -38,3 +46,8 @@ def conv_tag(v):
 def muladd_tag(v):
     wE, wi, wa, r = v
     return f"e{wE}m{wi}_a{wa}{_sfx(r)}"
+
+
+def pool_tag(v):
+    wE, wi, wa, wo, r = v
+    return f"e{wE}m{wi}_a{wa}_o{wo}{_sfx(r)}"

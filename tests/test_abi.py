@@ -145,3 +145,25 @@ def test_python_binding_refuses_host_tensors(hf):
     import torch
     with pytest.raises(TypeError):
         hf.pack(torch.zeros(4, 32), (5, 3))
+
+
+def test_avgpool_argument_checks(hf):
+    L = hf.lib()
+    f54, f55, f44 = hf.fmt((5, 4)), hf.fmt((5, 5)), hf.fmt((4, 4))
+    ok = (FAKE, FAKE, 2, 7, 7, 64, f54, f54, f54, 0, None)
+    # shapes, formats and rounding mode are checked before anything else
+    for i, bad in ((2, 0), (3, 0), (4, -1), (5, 0), (9, 2)):
+        args = list(ok)
+        args[i] = bad
+        assert L.hobflops_avgpool(*args) == -1, (i, bad)
+    assert L.hobflops_avgpool(FAKE, FAKE, 1, 1 << 16, 1 << 16, 8, f54, f54, f54, 0, None) == -1
+    assert L.hobflops_avgpool(FAKE, FAKE, 1, 2, 2, 8, f54, f44, f54, 0, None) == -1   # wE differs
+    assert L.hobflops_avgpool(FAKE, FAKE, 1, 2, 2, 8, f55, f54, f54, 0, None) == -1   # acc narrower
+    assert L.hobflops_avgpool(FAKE, FAKE, 1, 2, 2, 8, f54, f55, f55, 0, None) == -2   # not generated
+    assert L.hobflops_avgpool(None, FAKE, 1, 2, 2, 8, f54, f54, f54, 0, None) == -1
+    assert L.hobflops_avgpool(FAKE, MISALIGNED, 1, 2, 2, 8, f54, f54, f54, 0, None) == -3
+    assert hf.avgpool_supported((5, 4), (5, 4), (5, 4))
+    assert hf.avgpool_supported((5, 4), (5, 5), (5, 4), round=hf.ROUND_TOWARD_ZERO)
+    assert not hf.avgpool_supported((5, 4), (5, 5), (5, 5))
+    ops = hf.avgpool_netlist_ops((5, 4), (5, 4), (5, 4))
+    assert ops["accum"] == hf.netlist_ops((5, 3), (5, 4))["accum"] and ops["scale"] > 0
