@@ -9,38 +9,35 @@ namespace hobflops {
 
 // float32 bits -> code of (wE, wF): the exact value rounded to nearest even
 // with an unbounded exponent, then range checked (no subnormals in the format).
+// Every case is computed and selected, with no branches, so that the 64 lanes
+// of a wave never split (a mix of specials and normals is common).
 __device__ __forceinline__ uint32_t quantize_bits(uint32_t bits, int wE, int wF) {
   const uint32_t s = bits >> 31;
   const uint32_t ef = (bits >> 23) & 0xFFu;
   const uint32_t fr = bits & 0x7FFFFFu;
   const int sh_x = wF + wE + 1, sh_s = wF + wE;
-  if (ef == 0xFFu) return fr ? (3u << sh_x) : ((2u << sh_x) | (s << sh_s));
-  if (ef == 0 && fr == 0) return s << sh_s;
-  uint32_t M;
-  int u;  // value = M * 2^(u - 23) with M in [2^23, 2^24)
-  if (ef) {
-    M = fr | 0x800000u;
-    u = (int)ef - 127;
-  } else {
-    const int lz = __clz(fr) - 8;  // fr < 2^23
-    M = fr << lz;
-    u = -126 - lz;
-  }
-  const int k = 23 - wF;  // dropped bits, 0..22
+  const uint32_t sgn = s << sh_s;
+  // significand M in [2^23, 2^24) and exponent u: value = M * 2^(u - 23);
+  // a subnormal float32 is normalised by its leading zeros
+  const int lz = __clz(fr | 1u) - 8;
+  const bool sub = ef == 0u;
+  const uint32_t M = sub ? (fr << lz) : (fr | 0x800000u);
+  int u = sub ? -126 - lz : (int)ef - 127;
+  const int k = 23 - wF;  // dropped bits, 1..22 (wF <= 22 for a 32-bit code)
   uint32_t q = M >> k;
-  if (k > 0) {
-    const uint32_t rem = M & ((1u << k) - 1u);
-    const uint32_t half = 1u << (k - 1);
-    if (rem > half || (rem == half && (q & 1u))) q += 1u;
-    if (q == (2u << wF)) {
-      q >>= 1;
-      u += 1;
-    }
-  }
+  const uint32_t rem = M & ((1u << k) - 1u);
+  const uint32_t half = 1u << (k - 1);
+  q += (rem > half || (rem == half && (q & 1u))) ? 1u : 0u;
+  const bool carry = q == (2u << wF);  // rounded up into the next binade
+  q = carry ? q >> 1 : q;
+  u += carry ? 1 : 0;
   const int Eb = u + (1 << (wE - 1)) - 1;
-  if (Eb > (1 << wE) - 1) return (2u << sh_x) | (s << sh_s);
-  if (Eb < 0) return s << sh_s;
-  return (1u << sh_x) | (s << sh_s) | ((uint32_t)Eb << wF) | (q & ((1u << wF) - 1u));
+  const uint32_t inf = (2u << sh_x) | sgn;
+  uint32_t code = (1u << sh_x) | sgn | ((uint32_t)Eb << wF) | (q & ((1u << wF) - 1u));
+  code = Eb > (1 << wE) - 1 ? inf : code;
+  code = Eb < 0 || (sub && fr == 0u) ? sgn : code;         // underflow, +-0
+  code = ef == 0xFFu ? (fr ? (3u << sh_x) : inf) : code;  // NaN, +-inf
+  return code;
 }
 
 // code of (wE, wF) -> float32 bits (exact unless wE = 8 reaches float32's
