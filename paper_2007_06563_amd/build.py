@@ -42,9 +42,61 @@ def _gen_sources_digest():
     return h.hexdigest()[:16]
 
 
-def netlist(kind, key, rnd, cache):
-    """Optimised circuit for one operator (rounding mode rnd: variants.RNE or
-    RTZ); cached per generator version."""
+# Netlists whose results may be non-canonical (they feed only the adder and
+# the accumulator), so that E and F of a non-normal result and the sign of a
+# NaN are free: the don't-care pass of gen.opt applies to them.
+_NONCANONICAL = ("accum", "prod")
+_CIRCUITS = {}  # (kind, key, rounding name) -> (optimised circuit, raw node count)
+
+
+def _build_circuit(kind, key, r):
+    """The operator circuit, optimised and mapped to LUT3 (module level so that
+    a process pool can run it)."""
+    if kind == "mac":
+        C = fp.mac_circuit(*key, rnd=r)
+    elif kind == "prod":
+        C = fp.product_circuit(*key, rnd=r)
+    elif kind == "accum":
+        C = fp.accumulate_circuit(*key, rnd=r)
+    elif kind == "epi":
+        wE, wa, wo, act = key
+        C = fp.convert_circuit(wE, wa, wo, relu=bool(act), canonical=True, rnd=r)
+    elif kind == "scale":
+        C = fp.mul_circuit(*key, canonical=True, rnd=r)
+    else:
+        C = fp.muladd_circuit(*key, rnd=r)
+    raw = C.n_nodes()
+    C = opt.optimize(C)
+    if kind in _NONCANONICAL:
+        wE, wFo = key[0], key[-1]
+        D = opt.dont_care_substitute(C, opt.noncanonical_care(wE, wFo))
+        if D.n_nodes() < C.n_nodes():
+            D = opt.optimize(D)
+            C = D if D.n_nodes() < C.n_nodes() else C
+    return C, raw
+
+
+def circuit(kind, key, r):
+    """Optimised circuit of one operator (memoised for this build)."""
+    k = (kind, tuple(key), r)
+    if k not in _CIRCUITS:
+        _CIRCUITS[k] = _build_circuit(kind, key, r)
+    return _CIRCUITS[k]
+
+
+def prepare_circuits(needed, jobs=None):
+    """Optimise the circuits in `needed` (kind, key, rounding name) in parallel."""
+    todo = [k for k in dict.fromkeys(needed) if k not in _CIRCUITS]
+    if not todo:
+        return
+    jobs = jobs or min(16, os.cpu_count() or 4)
+    with cf.ProcessPoolExecutor(jobs) as ex:
+        for k, res in zip(todo, ex.map(_build_circuit, *zip(*todo))):
+            _CIRCUITS[k] = res
+
+
+def _netlist_name(kind, key, rnd):
+    """(function name, rounding name) of an operator's netlist."""
     name = {"mac": "mac_e{}m{}_a{}", "epi": "epi_e{}m{}_o{}{}", "muladd": "muladd_e{}m{}_a{}",
             "prod": "prod_e{}m{}_a{}", "accum": "accum_e{}m{}", "scale": "scale_e{}m{}_o{}"}[kind]
     r = variants.RND_NAME[rnd]
@@ -54,32 +106,18 @@ def netlist(kind, key, rnd, cache):
         # a widening convert rounds nothing: one netlist serves both modes
         if wo >= wa:
             r, sfx = "rne", ""
-        fname = name.format(wE, wa, wo, "_relu" if act else "") + sfx
-    else:
-        fname = name.format(*key) + sfx
+        return name.format(wE, wa, wo, "_relu" if act else "") + sfx, r
+    return name.format(*key) + sfx, r
+
+
+def netlist(kind, key, rnd, cache):
+    """Emitted netlist of one operator (rounding mode rnd: variants.RNE or
+    RTZ); cached per generator version."""
+    fname, r = _netlist_name(kind, key, rnd)
     if fname in cache:
         return fname, cache[fname]
-    if kind == "mac":
-        C = fp.mac_circuit(*key, rnd=r)
-        text_kw = {"in_place": "acc"}
-    elif kind == "prod":
-        C = fp.product_circuit(*key, rnd=r)
-        text_kw = {}
-    elif kind == "accum":
-        C = fp.accumulate_circuit(*key, rnd=r)
-        text_kw = {"in_place": "acc"}
-    elif kind == "epi":
-        wE, wa, wo, act = key
-        C = fp.convert_circuit(wE, wa, wo, relu=bool(act), canonical=True, rnd=r)
-        text_kw = {}
-    elif kind == "scale":
-        C = fp.mul_circuit(*key, canonical=True, rnd=r)
-        text_kw = {}
-    else:
-        C = fp.muladd_circuit(*key, rnd=r)
-        text_kw = {}
-    raw = C.n_nodes()
-    C = opt.optimize(C)
+    C, raw = circuit(kind, key, r)
+    text_kw = {"in_place": "acc"} if kind in ("mac", "accum") else {}
     entry = {"text": emit.emit_function(C, fname, **text_kw), "ops": emit.op_count(C),
              "raw_nodes": raw}
     cache[fname] = entry
@@ -106,8 +144,8 @@ def split_asm(wE, wi, wa, rnd, cache):
     if key not in cache:
         r = variants.RND_NAME[rnd]
         nin, nacc = nb(wE, wi), nb(wE, wa)
-        acc_c = opt.optimize(fp.accumulate_circuit(wE, wa, rnd=r))
-        prod_c = opt.optimize(fp.product_circuit(wE, wi, wa, rnd=r))
+        acc_c = circuit("accum", (wE, wa), r)[0]
+        prod_c = circuit("prod", (wE, wi, wa), r)[0]
         try:
             text, stats = asmgen.split_functions(acc_c, prod_c, nin, nacc,
                                                  split_batch(asmgen.pad4(nacc)),
@@ -129,6 +167,29 @@ def generate(verbose=True):
             cache = data["netlists"]
     files = []
     reg_conv, reg_mul = [], []
+    # every circuit whose netlist or split assembly is not cached, optimised in
+    # parallel first
+    needed = []
+    for wE, wi, wa, wo, act, rnd in variants.CONV_VARIANTS:
+        r = variants.RND_NAME[rnd]
+        for kind, key in (("mac", (wE, wi, wa)), ("epi", (wE, wa, wo, act)),
+                          ("prod", (wE, wi, wa)), ("accum", (wE, wa))):
+            fname, rr = _netlist_name(kind, key, rnd)
+            if fname not in cache:
+                needed.append((kind, key, rr))
+        skey = (f"split_e{wE}m{wi}_a{wa}{variants._sfx(rnd)}"
+                f"_s{SPLIT_SLOTS}_{SPLIT_SCHEDULE}_{SPLIT_SYNC}")
+        if skey not in cache:
+            needed += [("accum", (wE, wa), r), ("prod", (wE, wi, wa), r)]
+    for wE, wi, wa, rnd in variants.MULADD_VARIANTS:
+        if _netlist_name("muladd", (wE, wi, wa), rnd)[0] not in cache:
+            needed.append(("muladd", (wE, wi, wa), variants.RND_NAME[rnd]))
+    for wE, wi, wa, wo, rnd in variants.POOL_VARIANTS:
+        for kind, key in (("accum", (wE, wa)), ("scale", (wE, wa, wo))):
+            fname, rr = _netlist_name(kind, key, rnd)
+            if fname not in cache:
+                needed.append((kind, key, rr))
+    prepare_circuits(needed)
     for v in variants.CONV_VARIANTS:
         wE, wi, wa, wo, act, rnd = v
         tag = variants.conv_tag(v)

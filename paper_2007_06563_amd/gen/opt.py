@@ -17,10 +17,18 @@ one instruction (gfx950 ``v_bitop3_b32``):
   five signals can be written as g(h(S), T) -- two LUTs, h over at most three
   of the signals and g over h and the other (at most two) -- while the part
   of its cone that nothing else uses holds more than two LUTs, gets that
-  decomposition.
+  decomposition;
+* substitution under don't-cares (``dont_care_substitute``): a node becomes a
+  constant or an earlier signal wherever the two differ only on input
+  patterns at which no output bit that matters can see the difference. Every
+  input pattern is simulated, so the result is exact; it applies to circuits
+  of at most 24 input bits.
 """
 import itertools
 
+import numpy as np
+
+from . import sim
 from .circuit import Circuit, normalize, tt_mask, tt_var, tt_depends, tt_cofactor
 
 K = 3
@@ -396,3 +404,143 @@ def optimize(C: Circuit, max_iter=8, verbose=False):
             break
         best = C
     return best
+
+
+def _node_values(C, planes):
+    """Value of every node (uint64 word arrays) for input planes in port order."""
+    v = {0: np.zeros_like(planes[0])}
+    k = 0
+    for _, lits in C.inputs:
+        for l in lits:
+            v[l >> 1] = planes[k]
+            k += 1
+    for n in range(1, len(C.fanins)):
+        if not C.is_input[n]:
+            fan = C.fanins[n]
+            v[n] = sim._lut(C.tts[n], len(fan), [v[f] for f in fan])
+    return v
+
+
+def _out_values(C, v):
+    return [~v[l >> 1] if l & 1 else v[l >> 1] for _, lits in C.outputs for l in lits]
+
+
+def _visible(C, v, n, new, care, outs, fanout):
+    """Patterns at which replacing node n's value by `new` changes a cared-for
+    output bit (the transitive fan-out of n re-evaluated)."""
+    w = {n: new}
+    stack, seen = [n], {n}
+    order = []
+    while stack:
+        m = stack.pop()
+        for u in fanout[m]:
+            if u not in seen:
+                seen.add(u)
+                order.append(u)
+                stack.append(u)
+    for u in sorted(order):
+        fan = C.fanins[u]
+        w[u] = sim._lut(C.tts[u], len(fan), [w.get(f, v[f]) for f in fan])
+    diff = np.zeros_like(new)
+    i = 0
+    for _, lits in C.outputs:
+        for l in lits:
+            m = l >> 1
+            if m in w:
+                nv = ~w[m] if l & 1 else w[m]
+                diff |= (nv ^ outs[i]) & care[i]
+            i += 1
+    return diff
+
+
+def dont_care_substitute(C: Circuit, care_fn, max_inputs=24, samples=1 << 15, seed=1):
+    """Replace nodes by a constant or by an earlier signal (either polarity)
+    where no cared-for output can tell the difference.
+
+    care_fn(outputs) -> one mask per output bit (word arrays like the
+    outputs): the patterns at which that bit matters; it is evaluated on the
+    circuit as given, whose outputs the masks then describe. Candidates are
+    screened on random patterns and every substitution is checked on all
+    2^inputs patterns before it is kept."""
+    nin = sum(len(l) for _, l in C.inputs)
+    if nin > max_inputs or nin < 6:
+        return C
+    full = sim.exhaustive_planes(nin)
+    g = np.random.default_rng(seed)
+
+    def sample(count):
+        idx = g.integers(0, 1 << nin, count)
+        planes = []
+        for b in range(nin):
+            bits = ((idx >> b) & 1).astype(np.uint8)
+            planes.append(np.packbits(bits.reshape(-1, 64), axis=1, bitorder="little")
+                          .view(np.uint64).reshape(-1))
+        return planes
+
+    # two random samples screen candidates before the exhaustive check
+    samp, mid = sample(samples), sample(samples * 16)
+    care_full = care_fn(_out_values(C, _node_values(C, full)))
+    care_samp = care_fn(_out_values(C, _node_values(C, samp)))
+    care_mid = care_fn(_out_values(C, _node_values(C, mid)))
+    changed = True
+    while changed:
+        changed = False
+        N = len(C.fanins)
+        fanout = {m: [] for m in range(N)}
+        for m in range(1, N):
+            for f in C.fanins[m]:
+                fanout[f].append(m)
+        vs = _node_values(C, samp)
+        outs_s = _out_values(C, vs)
+        vm = outs_m = vf = outs_f = None
+        # screen every node: the sample patterns where its value matters
+        for n in range(N - 1, 0, -1):
+            if C.is_input[n]:
+                continue
+            cs = _visible(C, vs, n, ~vs[n], care_samp, outs_s, fanout)
+            t = vs[n]
+            cands = []
+            if not (t & cs).any():
+                cands.append(0)                      # constant 0
+            if not (~t & cs).any():
+                cands.append(1)                      # constant 1
+            for m in range(1, n):
+                if not ((vs[m] ^ t) & cs).any():
+                    cands.append(2 * m)
+                elif not ((~vs[m] ^ t) & cs).any():
+                    cands.append(2 * m + 1)
+            if not cands:
+                continue
+            if vm is None:
+                vm = _node_values(C, mid)
+                outs_m = _out_values(C, vm)
+
+            def survives(vals, care, outs, lit):
+                base = vals[lit >> 1] if lit >> 1 else np.zeros_like(vals[n])
+                new = ~base if lit & 1 else base
+                return not _visible(C, vals, n, new, care, outs, fanout).any()
+
+            cands = [lit for lit in cands if survives(vm, care_mid, outs_m, lit)]
+            if cands and vf is None:
+                vf = _node_values(C, full)
+                outs_f = _out_values(C, vf)
+            for lit in cands:
+                if survives(vf, care_full, outs_f, lit):
+                    D = rebuild(C, subst={n: lit})
+                    if D.n_nodes() < C.n_nodes():
+                        C, changed = D, True
+                        break
+            if changed:
+                break
+    return C
+
+
+def noncanonical_care(wE, wF):
+    """Output care masks of an operator whose result may be non-canonical:
+    E and F matter only for a normal result, the sign unless it is NaN."""
+    def care(outs):
+        x0, x1 = outs[wE + wF + 1], outs[wE + wF + 2]
+        normal, notnan = x0 & ~x1, ~(x0 & x1)
+        every = np.full_like(x0, np.uint64(0xFFFFFFFFFFFFFFFF))
+        return [normal] * (wE + wF) + [notnan, every, every]
+    return care
