@@ -379,6 +379,14 @@ def main():
     lane_ops = macs / 32.0 * G          # 32 MACs per 32-bit word operation
     achieved = lane_ops / (conv_ms * 1e-3)
     waves = ((P + 63) // 64) * ((s.M + 31) // 32)
+    if algo == hf.ALGO_SPLIT:
+        # each accumulator wave has a SIMD of its own; its chain of taps x
+        # adder instructions, one every ISSUE_CLOCKS at the nominal clock,
+        # bounds the kernel's time and hence its share of the peak
+        chain_s = s.KH * s.KW * s.C * ops["accum"] * ISSUE_CLOCKS / CLOCK_HZ
+        issue_ceiling = min(1.0, lane_ops / chain_s / PEAK_LANE_OPS)
+    else:
+        issue_ceiling = min(1.0, waves * SINGLE_WAVE_SHARE / N_SIMD)
     pack_bytes = (s.N * s.H * s.W * s.C + s.KH * s.KW * s.C * s.M) * 4 + \
         (p_ifm.numel() + p_w.numel()) * 4
     d_codes = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, IN_FMT, ACC_FMT,
@@ -411,8 +419,7 @@ def main():
                      "kernel": "conv2d_split_kernel" if algo == hf.ALGO_SPLIT else "conv2d_kernel",
                      "ops_per_mac_word": G,
                      "kernel_ms": conv_ms,
-                     "issue_ceiling": min(1.0, waves * SINGLE_WAVE_SHARE / N_SIMD) if algo ==
-                     hf.ALGO_FUSED else None},
+                     "issue_ceiling": issue_ceiling},
         "pct_valu_peak": 100.0 * achieved / PEAK_LANE_OPS,
         "conv_gmacs": macs / (conv_ms * 1e-3) / 1e9,
         "pack_ms": pack_ms,

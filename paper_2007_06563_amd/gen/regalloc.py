@@ -270,6 +270,68 @@ def allocate(C, in_ports, out_ports, pool, order=None):
         if not improved:
             break
 
+    # ---- annealing: random single moves (a value with its tied partner),
+    # accepted when they do not add conflicts or, with falling probability,
+    # when they do; the best colouring seen is kept (fixed seed: the result
+    # is reproducible)
+    # A move recolours one value; within a port whose block is full it swaps
+    # the banks of two of the port's bits instead.
+    rng = np.random.default_rng(12345)
+    mov = sorted(movable)
+    members = defaultdict(list)
+    for n in mov:
+        g = cap_of.get(n) or cap_of.get(partner.get(n))
+        if g is not None:
+            members[g].append(n)
+
+    def with_partner(n):
+        return [n, partner[n]] if n in partner else [n]
+
+    def set_color(ns, c):
+        for m in ns:
+            color[m] = c
+
+    cur = sum(bad(u) for u in nodes)
+    best_c, best_color = cur, dict(color)
+    steps = 60 * len(mov) if cur else 0
+    for step in range(steps):
+        if best_c == 0:
+            break
+        temp = 0.6 * (1.0 - step / steps) + 0.02
+        f = mov[int(rng.integers(len(mov)))]
+        grp = cap_of.get(f) or cap_of.get(partner.get(f))
+        old_c = color[f]
+        if grp is not None and capacity[grp][old_c] == 0 and rng.random() < 0.5:
+            g2 = members[grp][int(rng.integers(len(members[grp])))]
+            c = color[g2]
+            if c == old_c:
+                continue
+            moved = [(with_partner(f), old_c, c), (with_partner(g2), c, old_c)]
+        else:
+            c = int(rng.integers(NBANK))
+            if c == old_c or (grp is not None and capacity[grp][c] == 0):
+                continue
+            moved = [(with_partner(f), old_c, c)]
+        touched = set()
+        for ns, _, _ in moved:
+            for m in ns:
+                touched |= set(users[m])
+        before = sum(bad(u) for u in touched)
+        for ns, _, new in moved:
+            set_color(ns, new)
+        delta = sum(bad(u) for u in touched) - before
+        if delta <= 0 or rng.random() < np.exp(-delta / temp):
+            cur += delta
+            if grp is not None and len(moved) == 1:
+                capacity[grp][c] -= 1
+                capacity[grp][old_c] += 1
+            if cur < best_c:
+                best_c, best_color = cur, dict(color)
+        else:
+            for ns, old, _ in moved:
+                set_color(ns, old)
+    color = best_color
+
     # ---- place port bits
     pin, pout = {}, {}
     reg = {}
