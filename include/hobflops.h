@@ -91,6 +91,28 @@ int hobflops_plane_words(int64_t rows, int64_t len, hobflops_fmt f, int64_t* wor
 int hobflops_pack(const void* src, int kind, int64_t rows, int64_t len, hobflops_fmt f,
                   uint32_t* planes, void* stream);
 
+/* One tensor of hobflops_pack_batch: the arguments of a hobflops_pack call
+ * other than the format and the stream. */
+typedef struct {
+  const void* src;
+  int kind;
+  int64_t rows;
+  int64_t len;
+  uint32_t* planes;
+} hobflops_pack_job;
+
+/* hobflops_pack of several tensors of one format in few kernel launches: one
+ * per 8 jobs (a job of more than 2^30 values counts as several). Before the
+ * paper's first layer both the IFM and the kernels are transformed (Sec. 3.4);
+ * packed together they take one launch instead of two. jobs: host array of
+ * count entries (count >= 0; jobs may be NULL when count is 0), read before
+ * the call returns. Every job is checked as hobflops_pack checks its
+ * arguments, all before anything is launched, so that an error launches
+ * nothing; jobs with no values are skipped. The results are those of one
+ * hobflops_pack call per job; a job's planes must not overlap the src or the
+ * planes of another job. */
+int hobflops_pack_batch(const hobflops_pack_job* jobs, int count, hobflops_fmt f, void* stream);
+
 /* Unpack (paper Sec. 3.4: transformed back to floats after the last layer).
  * planes: PL32 tensor of format f; dst: rows*len elements, row-major; kind
  * HOBFLOPS_SRC_CODE_U32 writes codes (bits above NB zero), HOBFLOPS_SRC_F32

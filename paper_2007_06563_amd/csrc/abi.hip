@@ -6,6 +6,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <vector>
+
 #include "hobflops.h"
 #include "pack.hpp"
 #include "registry.hpp"
@@ -137,13 +139,29 @@ int hobflops_plane_words(int64_t rows, int64_t len, hobflops_fmt f, int64_t* wor
 
 int hobflops_pack(const void* src, int kind, int64_t rows, int64_t len, hobflops_fmt f,
                   uint32_t* planes, void* stream) {
-  if (rows < 0 || len < 0 || !fmt_ok(f)) return HOBFLOPS_EINVAL;
-  if (kind != HOBFLOPS_SRC_F32 && kind != HOBFLOPS_SRC_CODE_U32) return HOBFLOPS_EINVAL;
-  if (rows == 0 || len == 0) return HOBFLOPS_OK;
-  if (!src || !planes) return HOBFLOPS_EINVAL;
-  if (!aligned(src) || !aligned(planes)) return HOBFLOPS_EALIGN;
-  if ((len + 31) / 32 > INT32_MAX) return HOBFLOPS_EINVAL;
-  return hip_status(launch_pack(src, kind, rows, len, f.wE, f.wF, planes, (hipStream_t)stream));
+  const hobflops_pack_job job{src, kind, rows, len, planes};
+  return hobflops_pack_batch(&job, 1, f, stream);
+}
+
+int hobflops_pack_batch(const hobflops_pack_job* jobs, int count, hobflops_fmt f, void* stream) {
+  if (count < 0 || (count > 0 && !jobs) || !fmt_ok(f)) return HOBFLOPS_EINVAL;
+  std::vector<PackTensor> t;
+  t.reserve(count);
+  for (int n = 0; n < count; ++n) {
+    const hobflops_pack_job& j = jobs[n];
+    if (j.rows < 0 || j.len < 0) return HOBFLOPS_EINVAL;
+    if (j.kind != HOBFLOPS_SRC_F32 && j.kind != HOBFLOPS_SRC_CODE_U32) return HOBFLOPS_EINVAL;
+    if (j.rows == 0 || j.len == 0) continue;
+    if (!j.src || !j.planes) return HOBFLOPS_EINVAL;
+    if (!aligned(j.src) || !aligned(j.planes)) return HOBFLOPS_EALIGN;
+    if ((j.len + 31) / 32 > INT32_MAX) return HOBFLOPS_EINVAL;
+    int64_t words;  // rows * groups * NB must not overflow
+    if (hobflops_plane_words(j.rows, j.len, f, &words) != HOBFLOPS_OK) return HOBFLOPS_EINVAL;
+    t.push_back(PackTensor{j.src, j.kind, j.rows, j.len, j.planes});
+  }
+  if (t.empty()) return HOBFLOPS_OK;
+  return hip_status(
+      launch_pack_batch(t.data(), (int)t.size(), f.wE, f.wF, (hipStream_t)stream));
 }
 
 int hobflops_unpack(const uint32_t* planes, int64_t rows, int64_t len, hobflops_fmt f, int kind,

@@ -40,6 +40,38 @@ __device__ __forceinline__ uint32_t quantize_bits(uint32_t bits, int wE, int wF)
   return code;
 }
 
+// The same code as quantize_bits for wE <= 7, in fewer instructions. Such a
+// format's smallest normal is 2^-63 or larger, so every float32 subnormal (and
+// any value the add below might flush) lies below the range. For |x| in
+// [2^u, 2^(u+1)), C = 2^(u + 23 - wF) has the ulp 2^(u - wF) in its binade and
+// |x| + C stays in that binade, so the float32 add rounds |x| to wF fraction
+// bits, ties to even (the multiple index of C is even), and subtracting C
+// again is exact; a round-up into the next binade shows in the result's
+// exponent. The exponent field then moves by the bias difference, and the
+// sign of t tells an underflow. |x| is clamped to 2^100, which every such
+// format overflows, so that C stays finite; NaN is tested on the input.
+__device__ __forceinline__ uint32_t quantize_narrow(uint32_t bits, int wE, int wF) {
+  const uint32_t a = bits & 0x7FFFFFFFu;
+  const uint32_t ac = min(a, 0x71800000u);
+  const int k = 23 - wF;
+  const float C = __uint_as_float((ac & 0x7F800000u) + ((uint32_t)k << 23));
+  const float r = __fsub_rn(__fadd_rn(__uint_as_float(ac), C), C);
+  const int bias = (1 << (wE - 1)) - 1;
+  const int t = (int)(__float_as_uint(r) >> k) - ((127 - bias) << wF);
+  const int sh_x = wF + wE + 1;
+  const uint32_t sgn = (bits >> 31) << (wF + wE);
+  // the cases are selected with all-ones masks (arithmetic shifts of a
+  // difference's sign): as selects, the compiler turns some into branches
+  const uint32_t under = (uint32_t)(t >> 31);                           // t < 0
+  const uint32_t over = (uint32_t)(((1 << (wE + wF)) - 1 - t) >> 31);   // t >= 2^(wE+wF)
+  const uint32_t nan = (uint32_t)((int)(0x7F800000u - a) >> 31);        // a > 0x7F800000
+  uint32_t code = (1u << sh_x) | sgn | (uint32_t)t;
+  code = (code & ~under) | (sgn & under);                       // underflow, +-0
+  code = (code & ~over) | (((2u << sh_x) | sgn) & over);        // overflow, +-inf
+  code = (code & ~nan) | ((3u << sh_x) & nan);                  // NaN
+  return code;
+}
+
 // code of (wE, wF) -> float32 bits (exact unless wE = 8 reaches float32's
 // subnormal or overflow range, then rounded to nearest even).
 __device__ __forceinline__ uint32_t decode_bits(uint32_t code, int wE, int wF) {

@@ -3,13 +3,16 @@
 // value, an unpack the reverse.
 //
 // Pack: each lane quantises one value per pass; a pass holds two 32-value
-// groups (lanes 0-31 and 32-63), and NB ballots turn the wave's codes into the
-// NB plane words of both groups at once (the bit transpose of the paper's
-// bitslice layout, Sec. 3.2). Lane b then stores plane b of the first group and
-// lane 32+b plane b of the second, so a pass's stores are 2*NB consecutive
-// words. Unpack: lane j gathers bit j of the NB plane words of its group.
+// groups (lanes 0-31 and 32-63), and a 32 x 32 bit transpose across the lanes
+// of each half turns the 32 codes into the plane words of the group (the bit
+// transpose of the paper's bitslice layout, Sec. 3.2): lane b then holds plane
+// b, and lanes b < NB of both halves store, 2*NB consecutive words a pass.
+// Unpack: lanes b < NB load plane b of their group, and the same transpose
+// gives lane j the code of value j.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <algorithm>
 
 #include "codec.hpp"
 #include "pack.hpp"
@@ -22,62 +25,162 @@ namespace hobflops {
 // argument, so the plane loops unroll and their loads issue together.
 constexpr int kU = 4;
 
-// Row and column of group q: 32-bit arithmetic when the group count allows.
-template <bool kWide>
-__device__ __forceinline__ void group_rc(int64_t q, int G, int64_t& r, int64_t& c) {
-  if (kWide) {
+// Index of value j of group q in the [rows][len] source, and whether its
+// column 32g + j lies inside the row. With len a multiple of 32 the groups tile
+// the flat array, and no division is needed (kIdxDense); otherwise row and
+// group come from a division by G, in 32-bit arithmetic when the group count
+// allows (kIdxNarrow).
+constexpr int kIdxNarrow = 0, kIdxWide = 1, kIdxDense = 2;
+
+template <int kIdx>
+__device__ __forceinline__ int64_t value_index(int64_t q, int j, int G, int64_t len,
+                                               bool& in_row) {
+  if (kIdx == kIdxDense) {
+    in_row = true;
+    return q * 32 + j;
+  }
+  int64_t r, g;
+  if (kIdx == kIdxWide) {
     r = q / G;
-    c = q - r * G;
+    g = q - r * G;
   } else {
     const uint32_t q32 = (uint32_t)q, r32 = q32 / (uint32_t)G;
     r = r32;
-    c = q32 - r32 * (uint32_t)G;
+    g = q32 - r32 * (uint32_t)G;
   }
+  const int64_t col = g * 32 + j;
+  in_row = col < len;
+  return r * len + col;
 }
 
-template <int NB, bool kWide>
-__global__ __launch_bounds__(256) void pack_kernel(const void* __restrict__ src, int kind,
-                                                   int64_t len, int G, int wE, int wF,
-                                                   uint32_t* __restrict__ planes,
-                                                   int64_t ngroups) {
-  const int lane = threadIdx.x & 63;
-  const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
-  const int j = lane & 31;
-  constexpr uint32_t nbmask = NB >= 32 ? 0xFFFFFFFFu : ((1u << (NB & 31)) - 1u);
-  uint32_t raw[kU];
-  bool have[kU];
+// 32 x 32 bit transpose across each 32-lane half of a wave: lane j returns
+// the word whose bit i is bit j of lane i's x. Five stages d = 16, 8, 4, 2, 1
+// swap the off-diagonal d x d blocks of lane pairs (j, j ^ d): the lower lane
+// takes its partner's bits i (i & d == 0) into positions i + d, the upper one
+// its partner's bits i + d into positions i. A stage is one cross-lane read
+// (ds_swizzle, xor mode, no memory access), one rotate and one bit select; the
+// per-lane rotate amounts and masks are set up once (lane_transpose_setup).
+struct LaneT {
+  uint32_t rot[5], mask[5];
+};
+
+__device__ __forceinline__ LaneT lane_transpose_setup(int j) {
+  LaneT t;
+  constexpr uint32_t kLow[5] = {0x0000FFFFu, 0x00FF00FFu, 0x0F0F0F0Fu, 0x33333333u, 0x55555555u};
 #pragma unroll
-  for (int u = 0; u < kU; ++u) {  // group q = (wave * kU + u) * 2 + half
-    const int64_t q = (wave * kU + u) * 2 + (lane >> 5);
-    have[u] = false;
-    raw[u] = 0;
-    if (q < ngroups) {
-      int64_t r, g;
-      group_rc<kWide>(q, G, r, g);
-      const int64_t col = g * 32 + j;
-      if (col < len) {
-        raw[u] = ((const uint32_t*)src)[r * len + col];
-        have[u] = true;
-      }
-    }
+  for (int s = 0; s < 5; ++s) {
+    const int d = 16 >> s;
+    const bool upper = (j & d) != 0;
+    t.rot[s] = upper ? d : 32 - d;               // rotate right: by d, or left by d
+    t.mask[s] = upper ? kLow[s] : ~kLow[s];      // the positions taken from the partner
   }
+  return t;
+}
+
+template <int S>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t x) {
+  constexpr int d = 16 >> S;
+  // bit-mask mode: source lane ((i & 31) | 0) ^ d within each 32 lanes
+  return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, (d << 10) | 0x1F);
+}
+
+template <int U>
+__device__ __forceinline__ void lane_transpose(uint32_t (&x)[U], const LaneT& t) {
+#define HOBFLOPS_STAGE(S)                                                       \
+  {                                                                             \
+    uint32_t p[U];                                                              \
+    _Pragma("unroll") for (int u = 0; u < U; ++u) p[u] = xor_lane<S>(x[u]);     \
+    _Pragma("unroll") for (int u = 0; u < U; ++u) {                             \
+      const uint32_t r = __builtin_amdgcn_alignbit(p[u], p[u], t.rot[S]);       \
+      x[u] = (r & t.mask[S]) | (x[u] & ~t.mask[S]);                             \
+    }                                                                           \
+  }
+  HOBFLOPS_STAGE(0)
+  HOBFLOPS_STAGE(1)
+  HOBFLOPS_STAGE(2)
+  HOBFLOPS_STAGE(3)
+  HOBFLOPS_STAGE(4)
+#undef HOBFLOPS_STAGE
+}
+
+// A pack launch covers up to kMaxJobs ranges of groups, each of one tensor
+// (all in one format): range k holds groups [q0, q1) of its tensor and starts
+// at wave wave0 of the launch. A wave finds its range by comparing its index
+// with the wave0 of every range (uniform scalar work).
+constexpr int kMaxJobs = 8;
+struct PackRange {
+  const void* src;
+  uint32_t* planes;
+  int64_t len, q0, q1, wave0;
+  int G, kind, idx;  // groups per row, source kind, index mode
+};
+struct PackLaunch {
+  PackRange r[kMaxJobs];
+  int count;
+};
+
+// Source indices of a wave's kU passes: group q = q0 + (local wave * kU + u)
+// * 2 + half of range R; a lane without a value gets index 0 (loaded, then
+// ignored).
+template <int kIdx>
+__device__ __forceinline__ void value_indices(const PackRange& R, int64_t wave, int lane,
+                                              int64_t (&idx)[kU], bool (&have)[kU]) {
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
-    const int64_t q = (wave * kU + u) * 2 + (lane >> 5);
-    const uint32_t code =
-        have[u] ? (kind == 0 ? quantize_bits(raw[u], wE, wF) : (raw[u] & nbmask)) : 0u;
-    uint32_t mine = 0;
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const uint64_t m = __ballot((code >> b) & 1u);
-      const uint32_t half = (lane >> 5) ? (uint32_t)(m >> 32) : (uint32_t)m;
-      mine = (j == b) ? half : mine;
-    }
-    if (q < ngroups && j < NB) planes[q * NB + j] = mine;
+    const int64_t q = R.q0 + ((wave - R.wave0) * kU + u) * 2 + (lane >> 5);
+    bool in_row;
+    const int64_t i = value_index<kIdx>(q < R.q1 ? q : R.q0, lane & 31, R.G, R.len, in_row);
+    have[u] = q < R.q1 && in_row;
+    idx[u] = have[u] ? i : 0;
   }
 }
 
-template <int NB, bool kWide>
+template <int NB>
+__global__ __launch_bounds__(256) void pack_kernel(const PackLaunch L, int wE, int wF) {
+  const int lane = threadIdx.x & 63;
+  // the wave index as a wave-uniform value, so that the range lookup, the
+  // range's fields and the mode branches stay scalar
+  const int64_t wave = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int j = lane & 31;
+  constexpr uint32_t nbmask = NB >= 32 ? 0xFFFFFFFFu : ((1u << (NB & 31)) - 1u);
+  int k = 0;
+#pragma unroll
+  for (int t = 1; t < kMaxJobs; ++t) k = (t < L.count && wave >= L.r[t].wave0) ? t : k;
+  const PackRange& R = L.r[k];
+  int64_t idx[kU];
+  bool have[kU];
+  if (R.idx == kIdxDense)  // uniform branch
+    value_indices<kIdxDense>(R, wave, lane, idx, have);
+  else if (R.idx == kIdxWide)
+    value_indices<kIdxWide>(R, wave, lane, idx, have);
+  else
+    value_indices<kIdxNarrow>(R, wave, lane, idx, have);
+  // the kU loads together, every lane loading, with no branch between them: a
+  // load under a branch makes the compiler wait for all loads issued before it
+  uint32_t x[kU];
+#pragma unroll
+  for (int u = 0; u < kU; ++u) x[u] = ((const uint32_t*)R.src)[idx[u]];
+  // one uniform branch for the whole pass set
+  if (R.kind != 0) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) x[u] = have[u] ? (x[u] & nbmask) : 0u;
+  } else if (wE <= 7) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) x[u] = have[u] ? quantize_narrow(x[u], wE, wF) : 0u;
+  } else {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) x[u] = have[u] ? quantize_bits(x[u], wE, wF) : 0u;
+  }
+  // lane j of each half now holds plane j of its group
+  lane_transpose(x, lane_transpose_setup(j));
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const int64_t q = R.q0 + ((wave - R.wave0) * kU + u) * 2 + (lane >> 5);
+    if (q < R.q1 && j < NB) R.planes[q * NB + j] = x[u];
+  }
+}
+
+template <int NB, int kIdx>
 __global__ __launch_bounds__(256) void unpack_kernel(const uint32_t* __restrict__ planes,
                                                      int kind, int64_t len, int G, int wE,
                                                      int wF, void* __restrict__ dst,
@@ -85,42 +188,39 @@ __global__ __launch_bounds__(256) void unpack_kernel(const uint32_t* __restrict_
   const int lane = threadIdx.x & 63;
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int j = lane & 31;
-  uint32_t w[kU][NB];
+  uint32_t x[kU];
 #pragma unroll
-  for (int u = 0; u < kU; ++u) {  // every plane word of the lane's kU groups first
+  for (int u = 0; u < kU; ++u) {  // lane j < NB: plane j of its group (clamped load)
     const int64_t q = (wave * kU + u) * 2 + (lane >> 5);
-    const uint32_t* p = planes + (q < ngroups ? q : 0) * NB;
-#pragma unroll
-    for (int b = 0; b < NB; ++b) w[u][b] = p[b];
+    const uint32_t v = planes[(q < ngroups ? q : 0) * NB + min(j, NB - 1)];
+    x[u] = j < NB ? v : 0u;
   }
+  // the transpose is its own inverse: lane j now holds the code at column 32g + j
+  lane_transpose(x, lane_transpose_setup(j));
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
     const int64_t q = (wave * kU + u) * 2 + (lane >> 5);
     if (q >= ngroups) continue;
-    int64_t r, g;
-    group_rc<kWide>(q, G, r, g);
-    const int64_t col = g * 32 + j;
-    if (col >= len) continue;
-    uint32_t code = 0;
-#pragma unroll
-    for (int b = 0; b < NB; ++b) code |= ((w[u][b] >> j) & 1u) << b;
-    const int64_t i = r * len + col;
-    ((uint32_t*)dst)[i] = kind == 0 ? decode_bits(code, wE, wF) : code;
+    bool in_row;
+    const int64_t i = value_index<kIdx>(q, j, G, len, in_row);
+    if (!in_row) continue;
+    ((uint32_t*)dst)[i] = kind == 0 ? decode_bits(x[u], wE, wF) : x[u];
   }
 }
 
 namespace {
 
-// NB = 3 + wE + wF runs from 6 to 32.
-template <template <int, bool> class K, int NB = 6>
+// NB = 3 + wE + wF runs from 6 to 32; f gets the kernel types of the three
+// index modes.
+template <template <int, int> class K, int NB = 6>
 struct nb_dispatch {
   template <class F>
   static hipError_t run(int nb, F&& f) {
-    if (nb == NB) return f(K<NB, false>{}, K<NB, true>{});
+    if (nb == NB) return f(K<NB, kIdxNarrow>{}, K<NB, kIdxWide>{}, K<NB, kIdxDense>{});
     return nb_dispatch<K, NB + 1>::run(nb, f);
   }
 };
-template <template <int, bool> class K>
+template <template <int, int> class K>
 struct nb_dispatch<K, 33> {
   template <class F>
   static hipError_t run(int, F&&) {
@@ -128,55 +228,102 @@ struct nb_dispatch<K, 33> {
   }
 };
 
-template <int NB, bool W>
-struct PackK {
-  static constexpr auto fn = pack_kernel<NB, W>;
+template <int NB = 6>
+struct pack_nb {
+  static hipError_t run(int nb, unsigned blocks, hipStream_t stream, const PackLaunch& L, int wE,
+                        int wF) {
+    if (nb != NB) return pack_nb<NB + 1>::run(nb, blocks, stream, L, wE, wF);
+    hipLaunchKernelGGL(pack_kernel<NB>, dim3(blocks), dim3(256), 0, stream, L, wE, wF);
+    return hipGetLastError();
+  }
 };
-template <int NB, bool W>
+template <>
+struct pack_nb<33> {
+  static hipError_t run(int, unsigned, hipStream_t, const PackLaunch&, int, int) {
+    return hipErrorInvalidValue;
+  }
+};
+
+template <int NB, int M>
 struct UnpackK {
-  static constexpr auto fn = unpack_kernel<NB, W>;
+  static constexpr auto fn = unpack_kernel<NB, M>;
 };
 
 }  // namespace
 
-hipError_t launch_pack(const void* src, int kind, int64_t rows, int64_t len, int wE, int wF,
-                       uint32_t* planes, hipStream_t stream) {
-  const int NB = 3 + wE + wF;
-  const int64_t G = (len + 31) / 32;
-  const int64_t ngroups = rows * G;
+// Index mode of a tensor: dense when the row length is a multiple of 32, else
+// 32-bit division when the group count allows.
+static int index_mode(int64_t len, int64_t ngroups) {
+  if (len % 32 == 0) return kIdxDense;
+  return ngroups + 2 * kU >= ((int64_t)1 << 31) ? kIdxWide : kIdxNarrow;
+}
+
+// The unpack kernel of the tensor's index mode.
+template <template <int, int> class K, class... Args>
+static hipError_t launch_groups(int NB, int64_t len, int64_t ngroups, hipStream_t stream,
+                                Args... args) {
   const int64_t waves = (ngroups + 2 * kU - 1) / (2 * kU);
   const int64_t blocks = (waves + 3) / 4;
   if (blocks == 0) return hipSuccess;
-  const bool wide = ngroups + 2 * kU >= ((int64_t)1 << 31);
-  return nb_dispatch<PackK>::run(NB, [&](auto narrow_k, auto wide_k) {
-    if (wide)
-      hipLaunchKernelGGL(decltype(wide_k)::fn, dim3((unsigned)blocks), dim3(256), 0, stream, src,
-                         kind, len, (int)G, wE, wF, planes, ngroups);
+  const int mode = index_mode(len, ngroups);
+  return nb_dispatch<K>::run(NB, [&](auto narrow_k, auto wide_k, auto dense_k) {
+    if (mode == kIdxDense)
+      hipLaunchKernelGGL(decltype(dense_k)::fn, dim3((unsigned)blocks), dim3(256), 0, stream,
+                         args...);
+    else if (mode == kIdxWide)
+      hipLaunchKernelGGL(decltype(wide_k)::fn, dim3((unsigned)blocks), dim3(256), 0, stream,
+                         args...);
     else
-      hipLaunchKernelGGL(decltype(narrow_k)::fn, dim3((unsigned)blocks), dim3(256), 0, stream, src,
-                         kind, len, (int)G, wE, wF, planes, ngroups);
+      hipLaunchKernelGGL(decltype(narrow_k)::fn, dim3((unsigned)blocks), dim3(256), 0, stream,
+                         args...);
     return hipGetLastError();
   });
 }
 
+hipError_t launch_pack_batch(const PackTensor* t, int count, int wE, int wF, hipStream_t stream) {
+  // a range holds at most 2^25 groups and a launch at most 2^22 waves, so
+  // that the grid (64 threads a wave) stays far below 2^32 threads
+  constexpr int64_t kRangeGroups = (int64_t)1 << 25, kLaunchWaves = (int64_t)1 << 22;
+  const int NB = 3 + wE + wF;
+  PackLaunch L{};
+  int64_t waves = 0;
+  auto flush = [&]() -> hipError_t {
+    if (L.count == 0) return hipSuccess;
+    const hipError_t e = pack_nb<>::run(NB, (unsigned)((waves + 3) / 4), stream, L, wE, wF);
+    L = PackLaunch{};
+    waves = 0;
+    return e;
+  };
+  for (int n = 0; n < count; ++n) {
+    const int64_t G = (t[n].len + 31) / 32;
+    const int64_t ngroups = t[n].rows * G;
+    for (int64_t q0 = 0; q0 < ngroups; q0 += kRangeGroups) {
+      const int64_t q1 = std::min(ngroups, q0 + kRangeGroups);
+      const int64_t nw = (q1 - q0 + 2 * kU - 1) / (2 * kU);
+      if (L.count == kMaxJobs || waves + nw > kLaunchWaves) {
+        const hipError_t e = flush();
+        if (e != hipSuccess) return e;
+      }
+      L.r[L.count++] = PackRange{t[n].src, t[n].planes, t[n].len, q0, q1, waves, (int)G,
+                                 t[n].kind, index_mode(t[n].len, ngroups)};
+      waves += nw;
+    }
+  }
+  return flush();
+}
+
+hipError_t launch_pack(const void* src, int kind, int64_t rows, int64_t len, int wE, int wF,
+                       uint32_t* planes, hipStream_t stream) {
+  const PackTensor t{src, kind, rows, len, planes};
+  return launch_pack_batch(&t, 1, wE, wF, stream);
+}
+
 hipError_t launch_unpack(const uint32_t* planes, int64_t rows, int64_t len, int wE, int wF,
                          int kind, void* dst, hipStream_t stream) {
-  const int NB = 3 + wE + wF;
   const int64_t G = (len + 31) / 32;
   const int64_t ngroups = rows * G;
-  const int64_t waves = (ngroups + 2 * kU - 1) / (2 * kU);
-  const int64_t blocks = (waves + 3) / 4;
-  if (blocks == 0) return hipSuccess;
-  const bool wide = ngroups + 2 * kU >= ((int64_t)1 << 31);
-  return nb_dispatch<UnpackK>::run(NB, [&](auto narrow_k, auto wide_k) {
-    if (wide)
-      hipLaunchKernelGGL(decltype(wide_k)::fn, dim3((unsigned)blocks), dim3(256), 0, stream,
-                         planes, kind, len, (int)G, wE, wF, dst, ngroups);
-    else
-      hipLaunchKernelGGL(decltype(narrow_k)::fn, dim3((unsigned)blocks), dim3(256), 0, stream,
-                         planes, kind, len, (int)G, wE, wF, dst, ngroups);
-    return hipGetLastError();
-  });
+  return launch_groups<UnpackK>(3 + wE + wF, len, ngroups, stream, planes, kind, len, (int)G, wE,
+                                wF, dst, ngroups);
 }
 
 }  // namespace hobflops

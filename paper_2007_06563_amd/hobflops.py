@@ -43,7 +43,13 @@ class ConvDesc(ctypes.Structure):
                 ("algo", ctypes.c_int), ("ofm_kind", ctypes.c_int)]
 
 
-EXPORTS = ("hobflops_plane_words", "hobflops_pack", "hobflops_unpack", "hobflops_conv2d",
+class PackJob(ctypes.Structure):
+    _fields_ = [("src", ctypes.c_void_p), ("kind", ctypes.c_int), ("rows", ctypes.c_int64),
+                ("len", ctypes.c_int64), ("planes", ctypes.c_void_p)]
+
+
+EXPORTS = ("hobflops_plane_words", "hobflops_pack", "hobflops_pack_batch", "hobflops_unpack",
+           "hobflops_conv2d",
            "hobflops_conv2d_supported", "hobflops_muladd", "hobflops_muladd_supported",
            "hobflops_netlist_ops", "hobflops_avgpool", "hobflops_avgpool_supported",
            "hobflops_avgpool_netlist_ops", "hobflops_status_string")
@@ -60,6 +66,7 @@ def lib():
         vp, i64, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
         L.hobflops_plane_words.argtypes = [i64, i64, Fmt, ctypes.POINTER(i64)]
         L.hobflops_pack.argtypes = [vp, ci, i64, i64, Fmt, vp, vp]
+        L.hobflops_pack_batch.argtypes = [ctypes.POINTER(PackJob), ci, Fmt, vp]
         L.hobflops_unpack.argtypes = [vp, i64, i64, Fmt, ci, vp, vp]
         L.hobflops_conv2d.argtypes = [vp, vp, vp, ctypes.POINTER(ConvDesc), vp]
         L.hobflops_conv2d_supported.argtypes = [ctypes.POINTER(ConvDesc)]
@@ -133,6 +140,36 @@ def pack(src, f, rows=None, length=None, out=None):
         out = torch.empty(plane_shape(rows, length, f), dtype=torch.int32, device=src.device)
     _check(lib().hobflops_pack(_ptr(src), kind, rows, length, f, _ptr(out), _stream(src)))
     return out
+
+
+def pack_batch(items, f):
+    """Several pack() calls of one format in one launch (per 8 tensors).
+    items: sequence of (src, out) pairs with out None or a planes tensor, or
+    bare src tensors; each src packed along its last axis, as pack() does.
+    Returns the planes tensors in order. The launch goes to the current stream
+    of the first source's device."""
+    f = fmt(f)
+    jobs, outs = [], []
+    for it in items:
+        src, out = it if isinstance(it, (tuple, list)) else (it, None)
+        length = src.shape[-1] if src.dim() else 1
+        rows = src.numel() // max(length, 1)
+        if src.dtype == torch.float32:
+            kind = SRC_F32
+        elif src.dtype in (torch.int32, torch.uint32):
+            kind = SRC_CODE_U32
+        else:
+            raise TypeError("pack takes float32 values or int32 codes")
+        if out is None:
+            out = torch.empty(plane_shape(rows, length, f), dtype=torch.int32, device=src.device)
+        jobs.append(PackJob(_ptr(src).value, kind, rows, length, _ptr(out).value))
+        outs.append(out)
+    if not jobs:
+        return outs
+    arr = (PackJob * len(jobs))(*jobs)
+    first = items[0][0] if isinstance(items[0], (tuple, list)) else items[0]
+    _check(lib().hobflops_pack_batch(arr, len(jobs), f, _stream(first)))
+    return outs
 
 
 def unpack(planes, rows, length, f, kind="f32", out=None):

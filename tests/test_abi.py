@@ -112,6 +112,30 @@ def test_pack_unpack_argument_checks(hf):
     assert L.hobflops_unpack(FAKE, 4, 40, f, 0, MISALIGNED, None) == -3
 
 
+def test_pack_batch_argument_checks(hf):
+    L = hf.lib()
+    f = hf.Fmt(5, 3)
+    J = hf.PackJob
+
+    def batch(*jobs, fmt=f):
+        arr = (J * max(len(jobs), 1))(*jobs)
+        return L.hobflops_pack_batch(arr, len(jobs), fmt, None)
+
+    good = J(FAKE, 0, 4, 40, FAKE)
+    assert L.hobflops_pack_batch(None, 0, f, None) == 0     # nothing to do
+    assert L.hobflops_pack_batch(None, 2, f, None) == -1    # jobs missing
+    assert L.hobflops_pack_batch(None, -1, f, None) == -1
+    assert batch(good, fmt=hf.Fmt(5, 40)) == -1             # NB > 32
+    assert batch(J(None, 0, 0, 40, None), J(None, 1, 7, 0, None)) == 0  # empty jobs skipped
+    # a bad job anywhere fails the call before anything is launched (the good
+    # job's fake pointers would fault if it were)
+    assert batch(good, J(FAKE, 5, 4, 40, FAKE)) == -1       # kind
+    assert batch(good, J(FAKE, 0, -1, 40, FAKE)) == -1      # rows
+    assert batch(good, J(None, 0, 4, 40, FAKE)) == -1       # null source
+    assert batch(good, J(FAKE, 0, 4, 40, MISALIGNED)) == -3
+    assert batch(good, J(FAKE, 0, 1 << 40, 1 << 40, FAKE)) == -1  # size overflow
+
+
 def test_muladd_argument_checks(hf):
     L = hf.lib()
     a = hf.Fmt(5, 3)

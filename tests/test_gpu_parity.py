@@ -30,10 +30,29 @@ PACK_FORMATS = [(2, 1), (4, 2), (4, 3), (5, 2), (5, 3), (5, 4), (5, 10), (5, 11)
                 (8, 21), (7, 22), (6, 12)]
 
 
+def near_ties(seed, n, wE, wF):
+    """float32 values at, and one float32 ulp either side of, the midpoints
+    between neighbouring codes, over the format's exponent range and a few
+    binades past both ends (round-up carries, overflow, underflow)."""
+    g = np.random.default_rng([11, seed])
+    bias = (1 << (wE - 1)) - 1
+    e = g.integers(127 - bias - 3, 127 + bias + 4, n).clip(1, 254).astype(np.uint32)
+    k = 23 - wF
+    m = (g.integers(0, 1 << 23, n).astype(np.uint32) >> k << k) | np.uint32(1 << (k - 1))
+    m = (m.astype(np.int64) + g.integers(-1, 2, n)).astype(np.uint32) & np.uint32(0x7FFFFF)
+    s = g.integers(0, 2, n).astype(np.uint32) << 31
+    return (s | (e << 23) | m).view(np.float32)
+
+
+# (rows, length): ragged rows (3 groups per row, an odd number of groups) and
+# rows that are a whole number of groups (the groups tile the flat array)
+PACK_SHAPES = [(37, 70), (21, 96)]
+
+
+@pytest.mark.parametrize("rows,length", PACK_SHAPES)
 @pytest.mark.parametrize("wE,wF", PACK_FORMATS)
-def test_pack_unpack_float32(wE, wF):
+def test_pack_unpack_float32(wE, wF, rows, length):
     hf = need_gpu()
-    rows, length = 37, 70  # ragged: 3 groups per row, odd number of groups
     x = rand_f32(wE * 100 + wF, rows * length).reshape(rows, length)
     say(f"pack f32 fmt=({wE},{wF}) shape={x.shape}")
     planes = hf.pack(dev(x), (wE, wF))
@@ -49,11 +68,77 @@ def test_pack_unpack_float32(wE, wF):
     assert np.array_equal(vals.cpu().numpy().view(np.uint32), want_f.view(np.uint32))
 
 
+@pytest.mark.parametrize("rows,length", PACK_SHAPES)
+@pytest.mark.parametrize("wE,wF", PACK_FORMATS)
+def test_pack_rounding_ties_and_range_ends(wE, wF, rows, length):
+    hf = need_gpu()
+    x = near_ties(wE * 100 + wF, rows * length, wE, wF).reshape(rows, length)
+    say(f"pack ties fmt=({wE},{wF}) shape={x.shape}")
+    planes = hf.pack(dev(x), (wE, wF))
+    torch.cuda.synchronize()
+    want = orc.quantize_f32(x, wE, wF)
+    assert np.array_equal(planes.cpu().numpy().view(np.uint32), pack_codes(want, 3 + wE + wF))
+
+
+def _want_planes(src, wE, wF):
+    """Expected planes of a pack: oracle quantisation of float32 values, or the
+    codes' low NB bits."""
+    nbits = 3 + wE + wF
+    if src.dtype == np.float32:
+        codes = orc.quantize_f32(src, wE, wF)
+    else:
+        codes = src.view(np.uint32).astype(np.uint64) & np.uint64((1 << nbits) - 1)
+    return pack_codes(codes, nbits)
+
+
+@pytest.mark.parametrize("njobs", [5, 11])
+@pytest.mark.parametrize("wE,wF", [(5, 3), (8, 7), (4, 2)])
+def test_pack_batch_equals_single_packs(wE, wF, njobs):
+    """One launch per 8 jobs; dense, ragged, code, single-value and empty jobs
+    mixed. Each job's planes against the oracle."""
+    hf = need_gpu()
+    g = np.random.default_rng([13, wE, wF, njobs])
+    shapes = [(21, 96), (37, 70), (5, 1000), (1, 1), (0, 5), (3, 32), (9, 33), (2, 64), (4, 7),
+              (6, 200), (1, 31)][:njobs]
+    srcs = []
+    for t, (r, n) in enumerate(shapes):
+        if t % 3 == 2:
+            srcs.append(I.random_codes(600 + t, (r, n), 32).view(np.int32))
+        else:
+            srcs.append(rand_f32(500 + t, r * n).reshape(r, n))
+    say(f"pack_batch fmt=({wE},{wF}) jobs={njobs}")
+    outs = hf.pack_batch([dev(x) for x in srcs], (wE, wF))
+    torch.cuda.synchronize()
+    for x, o in zip(srcs, outs):
+        assert np.array_equal(o.cpu().numpy().view(np.uint32), _want_planes(x, wE, wF)), x.shape
+
+
+def test_pack_batch_splits_large_tensors():
+    """A tensor of more than 2^25 groups spans several ranges of a launch; the
+    rows next to the range boundaries and at both ends against the oracle."""
+    hf = need_gpu()
+    rows, length = (1 << 25) + 4099, 32       # one group per row
+    say(f"pack_batch large rows={rows} len={length}")
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    x = torch.randn((rows, length), generator=gen, device="cuda") * 3.0
+    small = dev(rand_f32(77, 40 * 45).reshape(40, 45))
+    o_big, o_small = hf.pack_batch([x, small], (5, 3))
+    torch.cuda.synchronize()
+    for r0 in (0, (1 << 25) - 3, rows - 5):
+        xs = x[r0:r0 + 5].cpu().numpy()
+        got = o_big[r0:r0 + 5].cpu().numpy().view(np.uint32)
+        assert np.array_equal(got, _want_planes(xs, 5, 3)), r0
+    assert np.array_equal(o_small.cpu().numpy().view(np.uint32),
+                          _want_planes(small.cpu().numpy(), 5, 3))
+    del x, o_big
+
+
+@pytest.mark.parametrize("length", [1000, 1024])
 @pytest.mark.parametrize("wE,wF", [(5, 3), (5, 4), (8, 8)])
-def test_pack_codes_round_trip(wE, wF):
+def test_pack_codes_round_trip(wE, wF, length):
     hf = need_gpu()
     nbits = 3 + wE + wF
-    rows, length = 5, 1000
+    rows = 5
     raw = I.random_codes(nbits, (rows, length), 32)  # garbage above NB too
     say(f"pack codes fmt=({wE},{wF})")
     planes = hf.pack(dev(raw.view(np.int32)), (wE, wF))
