@@ -42,6 +42,12 @@ TOP = 256
 ALIGN8 = ".p2align 3"
 
 
+def lgkm(n):
+    """A wait count for s_waitcnt lgkmcnt: the field holds at most 15, and a
+    smaller count only waits for more (LDS operations complete in order)."""
+    return min(n, 15)
+
+
 def pad4(n):
     return (n + 3) & ~3
 
@@ -185,7 +191,7 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
                 out += reads(slot, k)
             out += [f"L%=_go{slot}:"]
         for k in range(K):
-            out.append(f"s_waitcnt lgkmcnt({(K - 1 - k) * kstride})")
+            out.append(f"s_waitcnt lgkmcnt({lgkm((K - 1 - k) * kstride)})")
             if early and k == K - 1:
                 # every product of this batch is in registers: release the
                 # slot, then request the next batch's counter and entry 0
@@ -249,7 +255,7 @@ static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], cons
                 k = e[1]
                 last = max(i for i, x in enumerate(inflight) if x == ("r", slot, k))
                 newer = len(inflight) - 1 - last
-                body.append(f"s_waitcnt lgkmcnt({newer})")
+                body.append(f"s_waitcnt lgkmcnt({lgkm(newer)})")
                 inflight = inflight[last + 1:]
                 body += netlist(k)
         carried = inflight
@@ -307,7 +313,7 @@ def _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot, entry_
         m = {w0: wk for w0, wk in zip(W[0], W[k])}
         m.update({p0: pj for p0, pj in zip(PB[0], PB[k % 2])})
         out = [ALIGN8] + [f"v_bfe_i32 v{r}, %[x{b}], {creg}, 1" for b, r in enumerate(xregs)]
-        out.append(f"s_waitcnt lgkmcnt({wait})")
+        out.append(f"s_waitcnt lgkmcnt({lgkm(wait)})")
         out += [ALIGN8] + _rename(plines, m)
         out.append("s_nop 4")  # VALU results -> LDS store data
         for j in range(kstride):

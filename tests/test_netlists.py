@@ -225,9 +225,10 @@ def test_split_asm_allocation(wE, wi, wa):
                 assert np.array_equal(regs[r], w), (C.name, grp, r)
 
 
+@pytest.mark.parametrize("K", [4, 6])
 @pytest.mark.parametrize("sync", ["barrier", "pairs"])
 @pytest.mark.parametrize("wE,wi,wa", [(5, 3, 4), (5, 4, 5)])
-def test_split_asm_text(wE, wi, wa, sync):
+def test_split_asm_text(wE, wi, wa, sync, K):
     """Shape of the generated accumulator loop: one barrier per batch, or
     (pairs) none but a bounded counter wait and a consumed-count store per
     batch; wait counts within the 4-bit field; registers within v96..v255."""
@@ -235,7 +236,7 @@ def test_split_asm_text(wE, wi, wa, sync):
     nin, nacc = nbits(wE, wi), nbits(wE, wa)
     acc_c = optimized("accumulate_circuit", wE, wa)
     prod_c = optimized("product_circuit", wE, wi, wa)
-    text, _ = asmgen.split_functions(acc_c, prod_c, nin, nacc, 4, sync=sync)
+    text, _ = asmgen.split_functions(acc_c, prod_c, nin, nacc, K, sync=sync)
     loop = text[text.index("accum_loop("):text.index("kWSlot")]
     if sync == "barrier":
         assert loop.count("s_barrier") == 2
