@@ -132,6 +132,30 @@ def _conv_ops(d):
     return algo, (ops["mul"] + ops["accum"] if algo == hf.ALGO_SPLIT else ops["mac"])
 
 
+def pack_bench(reps):
+    """Pack and unpack alone, on the element-wise workload's first operand
+    (2^24 float32 values, (5,3)): one JSON line each, GB/s against 8 TB/s.
+    Algorithmic bytes: 4 B per value read + the planes written (pack), the
+    reverse for unpack."""
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    wE, wF = 5, 3
+    a = torch.from_numpy(I.fma_operands(I.FMA_FORMATS.index((wE, wF)))[0].reshape(1, -1)).to(dev)
+    n = a.numel()
+    pa = hf.pack(a, (wE, wF))
+    back = torch.empty_like(a)
+    nbytes = n * 4 + pa.numel() * 4
+    for name, fn in (("pack_kernel", lambda: hf.pack(a, (wE, wF), out=pa)),
+                     ("unpack_kernel", lambda: hf.unpack(pa, 1, n, (wE, wF), kind="f32",
+                                                         out=back))):
+        ms = _time(fn, reps, stream)
+        print(json.dumps({
+            "workload": f"{name.split('_')[0]} 2^24 float32 values, ({wE},{wF}), "
+                        f"{nbytes} algorithmic bytes", "kernel": name, "ms": ms,
+            "roofline": {"bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9, "peak": 8000.0,
+                         "unit": "GB/s", "frac": nbytes / (ms * 1e-3) / HBM_PEAK}}), flush=True)
+
+
 def suite(reps):
     """One JSON line per further workload: the element-wise sweep and
     pack/unpack against HBM, the mantissa sweep and the 13-layer stack
@@ -298,6 +322,9 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the one-line benchmark: the paper's MAC type sweep on the "
                          "MobileNets-shaped layer, one JSON line per type, rounding and batch")
+    ap.add_argument("--pack", action="store_true",
+                    help="instead of the one-line benchmark: pack and unpack alone on 2^24 "
+                         "values, one JSON line each (for the HBM counters)")
     ap.add_argument("--suite", action="store_true",
                     help="instead of the one-line benchmark: one JSON line per further workload "
                          "(element-wise sweep, mantissa sweep, 13-layer stack)")
@@ -311,6 +338,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.suite:
         suite(args.steps)
+        return
+    if args.pack:
+        pack_bench(args.steps)
         return
     if args.sweep:
         sweep(args.steps)

@@ -54,12 +54,15 @@ def test_fma_sweep_full_size(idx):
     pa, pb, pc = (hf.pack(dev(t.reshape(1, n)), (wE, wF)) for t in (a, b, c))
     r = hf.muladd(pa, pb, pc, n, (wE, wF), (wE, wa))
     got = codes_of(hf.unpack(r, 1, n, (wE, wa), kind="code"))[0]
+    got_f = hf.unpack(r, 1, n, (wE, wa), kind="f32").cpu().numpy().view(np.uint32)[0]
     g = np.random.default_rng([1, idx])
     sel = np.unique(np.concatenate([g.integers(0, n, 1 << 20), np.arange(n - 4096, n)]))
     qa, qb, qc = (threaded(orc.quantize_f32, t[sel], fixed=(wE, wF)) for t in (a, b, c))
     want = threaded(orc.muladd, qa, qb, qc, fixed=(wE, wF, wa))
     bad = np.flatnonzero(got[sel] != want)
     assert bad.size == 0, f"{bad.size} mismatches of {sel.size}; first at {sel[bad[0]]}"
+    want_f = orc.decode_f32(want, wE, wa).view(np.uint32)
+    assert np.array_equal(got_f[sel], want_f)
 
 
 def sample_points(shape_out, M, g, count):
