@@ -588,20 +588,38 @@ __global__ __launch_bounds__(256) void avgpool_kernel(const uint32_t* __restrict
   uint32_t acc[NACC];
 #pragma unroll
   for (int b = 0; b < NACC; ++b) acc[b] = 0u;  // +0
-  quad_t cur[NQ], nxt[NQ];
-  load(cur, src);
-  for (int i = 0; i < p.HW; ++i) {
-    // the next position's words are requested before this one is added
-    if (i + 1 < p.HW) load(nxt, src + (size_t)(i + 1) * step);
+  // Positions are requested kAhead ahead of their add, each into the register
+  // set its add has just read (the loop is unrolled by kAhead, so no set is
+  // copied): with a few waves in the whole launch, one position of lead left
+  // most of each load's latency exposed. Requests past the end reload the
+  // last position and are not used.
+  constexpr int kAhead = 4;
+  quad_t buf[kAhead][NQ];
+  const size_t last = (size_t)(p.HW - 1) * step;
+  auto pos_ptr = [&](int i) { return src + min((size_t)i * step, last); };
+#pragma unroll
+  for (int k = 0; k < kAhead; ++k) load(buf[k], pos_ptr(k));
+  auto add_pos = [&](quad_t (&q)[NQ], int i) {
+    // a scheduling barrier per position: the scheduler would otherwise hoist
+    // parts of later adds (those on x alone), and their waits would take in
+    // the loads requested ahead
+    __builtin_amdgcn_sched_barrier(0);
     uint32_t x[NACC];  // widened: fraction planes move up by DF, zeros below
 #pragma unroll
     for (int b = 0; b < DF; ++b) x[b] = 0u;
 #pragma unroll
-    for (int b = 0; b < NIN; ++b) x[DF + b] = cur[b / 4][b % 4];
+    for (int b = 0; b < NIN; ++b) x[DF + b] = q[b / 4][b % 4];
     V::add(acc, x);
+    load(q, pos_ptr(i + kAhead));
+  };
+  int i = 0;
+  for (; i + kAhead <= p.HW; i += kAhead) {
 #pragma unroll
-    for (int j = 0; j < NQ; ++j) cur[j] = nxt[j];
+    for (int k = 0; k < kAhead; ++k) add_pos(buf[k], i + k);
   }
+#pragma unroll
+  for (int k = 0; k < kAhead - 1; ++k)
+    if (i + k < p.HW) add_pos(buf[k], i + k);
   uint32_t sp[NACC], r[NOUT];
 #pragma unroll
   for (int b = 0; b < NACC; ++b) sp[b] = ((p.scale >> b) & 1u) ? 0xFFFFFFFFu : 0u;
