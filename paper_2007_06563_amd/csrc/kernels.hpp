@@ -199,8 +199,10 @@ __global__ __launch_bounds__(kConvBlock) void conv2d_kernel(const uint32_t* __re
       if (i < kRows * NIN) t[(i / NIN) * NINP + (i - (i / NIN) * NIN)] = stage[s];
     }
   };
-  auto read_row = [&](int buf, int c, uint32_t(&wv)[NIN]) {
-    const uint32_t* t = reinterpret_cast<const uint32_t*>(wtile[buf]) + c * NINP;
+  // the two tiles as one array of 2 * kRows rows
+  const uint32_t* tile = reinterpret_cast<const uint32_t*>(wtile);
+  auto read_row = [&](int row, uint32_t(&wv)[NIN]) {
+    const uint32_t* t = tile + row * NINP;
 #pragma unroll
     for (int b = 0; b < NIN; ++b) wv[b] = t[b];
   };
@@ -209,11 +211,24 @@ __global__ __launch_bounds__(kConvBlock) void conv2d_kernel(const uint32_t* __re
 #pragma unroll
   for (int b = 0; b < NACC; ++b) acc[b] = 0u;  // +0
 
+  // A layer with at most 2 * kRows weight rows per m-tile (a first layer of
+  // three channels has 27) keeps all of them in the tile, staged once: no
+  // per-chunk staging and no barrier per chunk.
+  const int T = p.KH * p.KW * p.C;
+  const bool resident = T <= 2 * kRows;
   uint32_t xn[NIN];
   bool xn_valid;
-  fetch_w(0, min(kRows, p.C));
+  if (resident) {
+    uint32_t* t = reinterpret_cast<uint32_t*>(wtile);
+    for (int i = tid; i < T * NIN; i += kConvBlock) {
+      const int row = i / NIN, b = i - row * NIN;
+      t[row * NINP + b] = wm[(size_t)row * wrow + b];
+    }
+  } else {
+    fetch_w(0, min(kRows, p.C));
+    store_w(0);
+  }
   load_ifm(0, 0, 0, xn, &xn_valid);
-  store_w(0);
   __syncthreads();
 
   int ky = 0, kx = 0, cg = 0;
@@ -232,7 +247,10 @@ __global__ __launch_bounds__(kConvBlock) void conv2d_kernel(const uint32_t* __re
     uint32_t xw[NIN];
 #pragma unroll
     for (int b = 0; b < NIN; ++b) xw[b] = xn_valid ? xn[b] : 0u;
-    fetch_w((ky2 * p.KW + kx2) * p.C + kRows * cg2, min(kRows, p.C - kRows * cg2));
+    // the chunk's first row in the tile
+    const int r0 = resident ? (ky * p.KW + kx) * p.C + kRows * cg : buf * kRows;
+    if (!resident)
+      fetch_w((ky2 * p.KW + kx2) * p.C + kRows * cg2, min(kRows, p.C - kRows * cg2));
     load_ifm(ky2, kx2, cg2, xn, &xn_valid);
 
     // Two rows in flight, ping-pong: the next row's LDS loads are issued
@@ -246,19 +264,21 @@ __global__ __launch_bounds__(kConvBlock) void conv2d_kernel(const uint32_t* __re
       V::mac(acc, wv, x);
     };
     uint32_t wa[NIN], wb[NIN];
-    read_row(buf, 0, wa);
+    read_row(r0, wa);
     int c = 0;
     for (; c + 2 <= nc; c += 2) {
-      read_row(buf, c + 1, wb);
+      read_row(r0 + c + 1, wb);
       __builtin_amdgcn_sched_barrier(0);
       mac_step(wa, c);
-      read_row(buf, c + 2 < nc ? c + 2 : c + 1, wa);
+      read_row(r0 + (c + 2 < nc ? c + 2 : c + 1), wa);
       __builtin_amdgcn_sched_barrier(0);
       mac_step(wb, c + 1);
     }
     if (c < nc) mac_step(wa, c);
-    store_w(buf ^ 1);
-    __syncthreads();
+    if (!resident) {
+      store_w(buf ^ 1);
+      __syncthreads();
+    }
     cg = cg2;
     kx = kx2;
     ky = ky2;
