@@ -23,11 +23,11 @@ __device__ __forceinline__ uint32_t quantize_bits(uint32_t bits, int wE, int wF)
   const bool sub = ef == 0u;
   const uint32_t M = sub ? (fr << lz) : (fr | 0x800000u);
   int u = sub ? -126 - lz : (int)ef - 127;
-  const int k = 23 - wF;  // dropped bits, 1..22 (wF <= 22 for a 32-bit code)
+  const int k = 23 - wF;  // dropped bits, 0..22 (none for wF = 23)
   uint32_t q = M >> k;
   const uint32_t rem = M & ((1u << k) - 1u);
-  const uint32_t half = 1u << (k - 1);
-  q += (rem > half || (rem == half && (q & 1u))) ? 1u : 0u;
+  const uint32_t half = k > 0 ? 1u << (k - 1) : 0u;
+  q += (k > 0 && (rem > half || (rem == half && (q & 1u)))) ? 1u : 0u;
   const bool carry = q == (2u << wF);  // rounded up into the next binade
   q = carry ? q >> 1 : q;
   u += carry ? 1 : 0;
@@ -55,7 +55,8 @@ __device__ __forceinline__ uint32_t quantize_narrow(uint32_t bits, int wE, int w
   const uint32_t ac = min(a, 0x71800000u);
   const int k = 23 - wF;
   const float C = __uint_as_float((ac & 0x7F800000u) + ((uint32_t)k << 23));
-  const float r = __fsub_rn(__fadd_rn(__uint_as_float(ac), C), C);
+  // wF = 23 keeps every bit: nothing to round
+  const float r = k > 0 ? __fsub_rn(__fadd_rn(__uint_as_float(ac), C), C) : __uint_as_float(ac);
   const int bias = (1 << (wE - 1)) - 1;
   const int t = (int)(__float_as_uint(r) >> k) - ((127 - bias) << wF);
   const int sh_x = wF + wE + 1;

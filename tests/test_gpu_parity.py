@@ -25,9 +25,10 @@ def rand_f32(seed, n, lo=-4.0, hi=4.0, specials=0.02):
     return I.inject_specials(x, g, specials)
 
 
-# NB = 3 + wE + wF must fit a 32-bit code: (8,21) and (7,22) are the widest
+# NB = 3 + wE + wF must fit a 32-bit code: (8,21), (7,22) and (6,23) are the
+# widest; wF = 23 keeps every float32 fraction bit (no rounding)
 PACK_FORMATS = [(2, 1), (4, 2), (4, 3), (5, 2), (5, 3), (5, 4), (5, 10), (5, 11), (8, 7), (8, 8),
-                (8, 21), (7, 22), (6, 12)]
+                (8, 21), (7, 22), (6, 12), (6, 23), (2, 23)]
 
 
 def near_ties(seed, n, wE, wF):
@@ -38,7 +39,9 @@ def near_ties(seed, n, wE, wF):
     bias = (1 << (wE - 1)) - 1
     e = g.integers(127 - bias - 3, 127 + bias + 4, n).clip(1, 254).astype(np.uint32)
     k = 23 - wF
-    m = (g.integers(0, 1 << 23, n).astype(np.uint32) >> k << k) | np.uint32(1 << (k - 1))
+    m = g.integers(0, 1 << 23, n).astype(np.uint32)
+    if k > 0:  # (wF = 23 has no midpoints: every float32 value is exact)
+        m = (m >> k << k) | np.uint32(1 << (k - 1))
     m = (m.astype(np.int64) + g.integers(-1, 2, n)).astype(np.uint32) & np.uint32(0x7FFFFF)
     s = g.integers(0, 2, n).astype(np.uint32) << 31
     return (s | (e << 23) | m).view(np.float32)
