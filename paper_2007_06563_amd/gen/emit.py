@@ -6,7 +6,8 @@ signal (Sec. 3.3). Here one signal is one 32-bit VGPR, i.e. the same bit of
 32 independent values, and every node is one VALU instruction: three-input
 nodes become ``__builtin_amdgcn_bitop3_b32`` with the node's truth table as
 the immediate, two-input nodes plain C operators (which the compiler selects
-as single VALU instructions).
+as single VALU instructions) or, in an aligned function, also
+``v_bitop3_b32`` (see emit_function).
 
 ``v_bitop3_b32 D, S0, S1, S2, imm`` computes, for every bit position, bit
 (S0*4 + S1*2 + S2) of imm. A node's truth table weights input i by 2**i, so
@@ -74,10 +75,16 @@ def output_polarity(C):
     return neg - pos
 
 
-def emit_function(C, fname, in_place=None):
+def emit_function(C, fname, in_place=None, aligned=False):
     """C++ text of one __device__ function. Inputs are const array references
     in port order; the output group is a reference array. If in_place names an
-    input group, the output overwrites that input array."""
+    input group, the output overwrites that input array.
+
+    aligned: two-input nodes also become ``v_bitop3_b32`` (with the constant 0
+    as S0), so that every node is one 8-byte instruction, and the run starts
+    at an 8-byte boundary (an alignment directive, then a scheduling barrier
+    that keeps the nodes after it). Otherwise two-input nodes are C operators,
+    which the compiler may select as 4-byte instructions."""
     from .circuit import tt_flip
     flipped = output_polarity(C)
     names = {}
@@ -112,6 +119,8 @@ def emit_function(C, fname, in_place=None):
         args = [names[f] for f in fan]
         if k == 3:
             expr = f"__builtin_amdgcn_bitop3_b32({args[2]}, {args[1]}, {args[0]}, 0x{tt:02x})"
+        elif k == 2 and aligned:
+            expr = f"__builtin_amdgcn_bitop3_b32(0u, {args[1]}, {args[0]}, 0x{tt:02x})"
         elif k == 2:
             expr = TWO_INPUT[tt].format(a=args[0], b=args[1])
         else:
@@ -128,7 +137,11 @@ def emit_function(C, fname, in_place=None):
                 val = ("~" if inv else "") + names[n]
             stores.append(f"  {group}[{b}] = {val};")
     head = f"static __device__ __forceinline__ void {fname}({', '.join(params)})\n{{"
-    return "\n".join([head] + loads + body + stores + ["}"]) + "\n"
+    # a run of 8-byte instructions issues at full rate only when it starts
+    # 8-byte aligned (the assembler pads with s_nop 0)
+    align = ['  asm volatile(".p2align 3");',
+             "  __builtin_amdgcn_sched_barrier(0);"] if aligned else []
+    return "\n".join([head] + loads + align + body + stores + ["}"]) + "\n"
 
 
 def op_count(C):
