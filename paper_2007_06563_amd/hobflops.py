@@ -106,6 +106,14 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _require(t, nbytes, name):
+    """The library reads and writes through raw pointers: a tensor smaller than
+    the call's extent is refused here, before any launch."""
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{name}: {have} bytes, the call needs {nbytes}")
+
+
 def _stream(t):
     return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
 
@@ -138,6 +146,7 @@ def pack(src, f, rows=None, length=None, out=None):
         raise TypeError("pack takes float32 values or int32 codes")
     if out is None:
         out = torch.empty(plane_shape(rows, length, f), dtype=torch.int32, device=src.device)
+    _require(out, 4 * plane_words(rows, length, f), "pack out")
     _check(lib().hobflops_pack(_ptr(src), kind, rows, length, f, _ptr(out), _stream(src)))
     return out
 
@@ -162,6 +171,7 @@ def pack_batch(items, f):
             raise TypeError("pack takes float32 values or int32 codes")
         if out is None:
             out = torch.empty(plane_shape(rows, length, f), dtype=torch.int32, device=src.device)
+        _require(out, 4 * plane_words(rows, length, f), "pack_batch out")
         jobs.append(PackJob(_ptr(src).value, kind, rows, length, _ptr(out).value))
         outs.append(out)
     if not jobs:
@@ -179,6 +189,8 @@ def unpack(planes, rows, length, f, kind="f32", out=None):
     if out is None:
         out = torch.empty((rows, length), dtype=torch.float32 if k == SRC_F32 else torch.int32,
                           device=planes.device)
+    _require(planes, 4 * plane_words(rows, length, f), "unpack planes")
+    _require(out, 4 * rows * length, "unpack out")
     _check(lib().hobflops_unpack(_ptr(planes), rows, length, f, k, _ptr(out), _stream(planes)))
     return out
 
@@ -205,6 +217,11 @@ def conv2d(ifm, w, d, out=None):
         else:
             out = torch.empty((d.N * OH * OW, d.M), device=ifm.device,
                               dtype=torch.float32 if d.ofm_kind == OFM_F32 else torch.int32)
+    if OH > 0 and OW > 0 and d.N > 0 and d.C > 0 and d.M > 0:
+        _require(ifm, 4 * plane_words(d.N * d.H * d.W, d.C, d.in_fmt), "conv2d ifm")
+        _require(w, 4 * plane_words(d.KH * d.KW * d.C, d.M, d.in_fmt), "conv2d w")
+        _require(out, 4 * (plane_words(d.N * OH * OW, d.M, d.out_fmt) if d.ofm_kind == OFM_PLANES
+                           else d.N * OH * OW * d.M), "conv2d out")
     _check(lib().hobflops_conv2d(_ptr(ifm), _ptr(w), _ptr(out), ctypes.byref(d), _stream(ifm)))
     return out
 
@@ -218,6 +235,9 @@ def muladd(a, b, c, n, in_fmt, acc_fmt, out=None, round=ROUND_NEAREST_EVEN):
     in_fmt, acc_fmt = fmt(in_fmt), fmt(acc_fmt)
     if out is None:
         out = torch.empty(plane_shape(1, n, acc_fmt), dtype=torch.int32, device=a.device)
+    for t, name in ((a, "a"), (b, "b"), (c, "c")):
+        _require(t, 4 * plane_words(1, n, in_fmt), f"muladd {name}")
+    _require(out, 4 * plane_words(1, n, acc_fmt), "muladd out")
     _check(lib().hobflops_muladd(_ptr(a), _ptr(b), _ptr(c), _ptr(out), n, in_fmt, acc_fmt, round,
                                  _stream(a)))
     return out
@@ -243,6 +263,9 @@ def avgpool(planes, N, H, W, C, in_fmt, acc_fmt, out_fmt, out=None, round=ROUND_
     in_fmt, acc_fmt, out_fmt = fmt(in_fmt), fmt(acc_fmt), fmt(out_fmt)
     if out is None:
         out = torch.empty(plane_shape(N, C, out_fmt), dtype=torch.int32, device=planes.device)
+    if N > 0 and H > 0 and W > 0 and C > 0:
+        _require(planes, 4 * plane_words(N * H * W, C, in_fmt), "avgpool planes")
+        _require(out, 4 * plane_words(N, C, out_fmt), "avgpool out")
     _check(lib().hobflops_avgpool(_ptr(planes), _ptr(out), N, H, W, C, in_fmt, acc_fmt, out_fmt,
                                   round, _stream(planes)))
     return out

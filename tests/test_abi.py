@@ -171,6 +171,38 @@ def test_python_binding_refuses_host_tensors(hf):
         hf.pack(torch.zeros(4, 32), (5, 3))
 
 
+def test_python_binding_refuses_short_buffers(hf):
+    """The library works on raw pointers; the binding refuses tensors smaller
+    than a call's extent before anything reaches the device (these tensors
+    are on the host, so a call that got past the check would fail with
+    TypeError instead)."""
+    import torch
+    i32 = torch.int32
+    with pytest.raises(ValueError, match="pack out"):
+        hf.pack(torch.zeros(4, 40), (5, 3), out=torch.zeros(4 * 2 * 11 - 1, dtype=i32))
+    with pytest.raises(ValueError, match="pack_batch out"):
+        hf.pack_batch([(torch.zeros(4, 40), torch.zeros(5, dtype=i32))], (5, 3))
+    with pytest.raises(ValueError, match="unpack planes"):
+        hf.unpack(torch.zeros(4 * 2 * 11 - 1, dtype=i32), 4, 40, (5, 3))
+    with pytest.raises(ValueError, match="unpack out"):
+        hf.unpack(torch.zeros(4 * 2 * 11, dtype=i32), 4, 40, (5, 3),
+                  out=torch.zeros(4 * 40 - 1))
+    d = hf.conv_desc(1, 4, 4, 40, 8, 3, 3, 1, 1, (5, 3), (5, 4), (5, 4))
+    ifm_words, w_words = 16 * 2 * 11, 9 * 40 * 1 * 11
+    with pytest.raises(ValueError, match="conv2d ifm"):
+        hf.conv2d(torch.zeros(ifm_words - 1, dtype=i32), torch.zeros(w_words, dtype=i32), d)
+    with pytest.raises(ValueError, match="conv2d w"):
+        hf.conv2d(torch.zeros(ifm_words, dtype=i32), torch.zeros(w_words - 1, dtype=i32), d)
+    with pytest.raises(ValueError, match="conv2d out"):
+        hf.conv2d(torch.zeros(ifm_words, dtype=i32), torch.zeros(w_words, dtype=i32), d,
+                  out=torch.zeros(16 * 12 - 1, dtype=i32))
+    with pytest.raises(ValueError, match="muladd b"):
+        hf.muladd(torch.zeros(11, dtype=i32), torch.zeros(10, dtype=i32),
+                  torch.zeros(11, dtype=i32), 32, (5, 3), (5, 4))
+    with pytest.raises(ValueError, match="avgpool planes"):
+        hf.avgpool(torch.zeros(10, dtype=i32), 1, 2, 2, 32, (5, 4), (5, 4), (5, 4))
+
+
 def test_avgpool_argument_checks(hf):
     L = hf.lib()
     f54, f55, f44 = hf.fmt((5, 4)), hf.fmt((5, 5)), hf.fmt((4, 4))
