@@ -94,6 +94,53 @@ def _want_planes(src, wE, wF):
     return pack_codes(codes, nbits)
 
 
+@pytest.mark.parametrize("wE,wF", [f for f in PACK_FORMATS if 3 + f[0] + f[1] <= 20])
+def test_unpack_every_code(wE, wF):
+    """Every code of the format (2^NB, non-canonical specials included) packed
+    from codes and unpacked to float32 and to codes, against the oracle's
+    decoder."""
+    hf = need_gpu()
+    nbits = 3 + wE + wF
+    codes = np.arange(1 << nbits, dtype=np.uint32).reshape(1, -1)
+    say(f"unpack every code fmt=({wE},{wF}) n={codes.size}")
+    planes = hf.pack(dev(codes.view(np.int32)), (wE, wF))
+    back = hf.unpack(planes, 1, codes.size, (wE, wF), kind="code")
+    vals = hf.unpack(planes, 1, codes.size, (wE, wF), kind="f32")
+    torch.cuda.synchronize()
+    assert np.array_equal(codes_of(back), codes.astype(np.uint64))
+    want = orc.decode_f32(codes.astype(np.uint64), wE, wF)
+    assert np.array_equal(vals.cpu().numpy().view(np.uint32), want.view(np.uint32))
+
+
+def test_pack_every_float32_pattern():
+    """All 2^32 float32 bit patterns through the pack kernel (and the unpack
+    to codes), against checksums of the oracle's codes per 2^28 patterns
+    (tests/golden/quantize_all_f32.json, written by
+    tests/golden/make_quantize_checksums.py from oracle/ alone)."""
+    import json
+    import os
+    hf = need_gpu()
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                       "quantize_all_f32.json")))
+    n = 1 << gold["chunk_bits"]
+    for key, chunks in gold["formats"].items():
+        wE, wF = (int(v) for v in key.split(","))
+        for c, want in enumerate(chunks):
+            say(f"pack every float32 pattern fmt=({wE},{wF}) chunk {c}")
+            first = c * n
+            i = torch.arange(first, first + n, dtype=torch.int64, device="cuda")
+            bits = torch.where(i >= (1 << 31), i - (1 << 32), i).to(torch.int32)
+            planes = hf.pack(bits.view(torch.float32).reshape(1, n), (wE, wF))
+            codes = hf.unpack(planes, 1, n, (wE, wF), kind="code").reshape(-1).to(torch.int64)
+            codes &= (1 << 32) - 1
+            got = []
+            for A, B, P in gold["hashes"]:
+                h = (A * (i % P) + B) % P
+                got.append(int(((((codes + 1) % P) * h) % P).sum().item() % P))
+            assert got == want, (key, c)
+            del i, bits, planes, codes, h
+
+
 @pytest.mark.parametrize("njobs", [5, 11])
 @pytest.mark.parametrize("wE,wF", [(5, 3), (8, 7), (4, 2)])
 def test_pack_batch_equals_single_packs(wE, wF, njobs):
