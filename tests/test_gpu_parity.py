@@ -210,6 +210,39 @@ def test_empty_pack_is_a_no_op():
     hf.pack(torch.empty((0, 5), device="cuda"), (5, 3), rows=0, length=5)
 
 
+def test_muladd_every_triple_of_codes():
+    """Every triple of codes of the small formats in
+    tests/golden/muladd_all_codes.json (written by
+    tests/golden/make_muladd_checksums.py from oracle/ alone): a = i mod 2^NB,
+    b = (i >> NB) mod 2^NB, c = i >> 2 NB, packed from codes, through
+    hobflops_muladd, the result codes' checksums per 2^24 triples against the
+    oracle's."""
+    import json
+    import os
+    hf = need_gpu()
+    gold = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                       "muladd_all_codes.json")))
+    n = 1 << gold["chunk_bits"]
+    for key, chunks in gold["cases"].items():
+        wE, wi, wa = (int(v) for v in key.split(",")[:3])
+        rnd = hf.ROUND_NEAREST_EVEN if key.endswith("rne") else hf.ROUND_TOWARD_ZERO
+        nb = 3 + wE + wi
+        for ch, want in enumerate(chunks):
+            say(f"muladd every triple {key} chunk {ch}")
+            i = torch.arange(ch * n, (ch + 1) * n, dtype=torch.int64, device="cuda")
+            ops = [((i >> (k * nb)) & ((1 << nb) - 1)).to(torch.int32).reshape(1, n)
+                   for k in range(3)]
+            pa, pb, pc = hf.pack_batch(ops, (wE, wi))
+            r = hf.muladd(pa, pb, pc, n, (wE, wi), (wE, wa), round=rnd)
+            codes = hf.unpack(r, 1, n, (wE, wa), kind="code").reshape(-1).to(torch.int64)
+            codes &= (1 << 32) - 1
+            got = []
+            for A, B, P in gold["hashes"]:
+                h = (A * (i % P) + B) % P
+                got.append(int(((((codes + 1) % P) * h) % P).sum().item() % P))
+            assert got == want, (key, ch)
+
+
 @pytest.mark.parametrize("v", variants.MULADD_VARIANTS, ids=variants.muladd_tag)
 def test_muladd_vs_oracle(v):
     hf = need_gpu()
