@@ -292,6 +292,24 @@ def run_conv(hf, ifm_codes, w_codes, stride, pad, wE, wi, wa, wo, act, algo=0, r
     return codes_of(out).reshape(N, OH, OW, M)
 
 
+@pytest.mark.parametrize("rnd", [0, 1], ids=["rne", "rtz"])
+@pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
+def test_conv_every_product_pair(algo, rnd):
+    """A one-tap convolution whose IFM positions are all 2^11 codes of (5,3)
+    and whose kernels are all 2^11 codes too: every (w, x) pair through the
+    multiplier, the add into +0 and the epilogue, against the oracle."""
+    hf = need_gpu()
+    nb = 11
+    codes = np.arange(1 << nb, dtype=np.uint64)
+    ifm = codes.reshape(1, 1, 1 << nb, 1)
+    w = codes.reshape(1, 1, 1, 1 << nb)
+    say(f"conv every product pair algo={algo} rnd={rnd}")
+    got = run_conv(hf, ifm, w, 1, 0, 5, 3, 4, 4, 0, algo, rnd)
+    want = orc.conv2d(ifm, w, 1, 0, 5, 3, 4, 4, rnd=orc.RTZ if rnd else orc.RNE)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{bad.size} mismatches; first at {bad[0]}"
+
+
 def test_small_conv_workload():
     """8x8x4 IFM, eight 3x3x4 kernels, (5,3) inputs, (5,4) accumulation."""
     hf = need_gpu()
