@@ -158,11 +158,17 @@ def split_asm(wE, wi, wa, rnd, cache):
         acc_c = circuit("accum", (wE, wa), r)[0]
         prod_c = circuit("prod", (wE, wi, wa), r)[0]
         cache[key] = {"text": None, "stats": {"unavailable": "no batch size fits"}}
-        for K in split_batches(asmgen.pad4(nacc)):
+        # the largest batch first; for each, the asm register windows from
+        # v96, else from v80, else the accumulator's from v48 (its role keeps
+        # few values of the compiler's; the multiplier's stays at v80)
+        bases = ((96, 96), (80, 80), (48, 80))
+        for K, (base, mul_base) in [(K, b) for K in split_batches(asmgen.pad4(nacc))
+                                    for b in bases]:
             try:
                 text, stats = asmgen.split_functions(acc_c, prod_c, nin, nacc, K,
-                                                     SPLIT_SLOTS, SPLIT_SCHEDULE, SPLIT_SYNC)
-                stats["batch"] = K
+                                                     SPLIT_SLOTS, SPLIT_SCHEDULE, SPLIT_SYNC,
+                                                     base=base, mul_base=mul_base)
+                stats["batch"], stats["base"] = K, [base, mul_base]
                 cache[key] = {"text": text, "stats": stats, "batch": K}
                 break
             except regalloc.AllocError as e:

@@ -23,9 +23,10 @@ reads two VGPRs of one bank (see gen/regalloc.py). The functions produced:
 * ``product_step(xw, c, wrow, entry)``: the same for one product (batches at a
   channel-word boundary and the last, partial batch).
 
-Port registers are fixed ranges from v96 upwards; the temporaries are the
-rest of v96..v255, declared clobbered, so the compiler's own values stay below
-or are not live across the blocks.
+Port registers are fixed ranges from v96 upwards (from v80, or for the
+accumulator from v48, for the widest formats, whose netlists need the room);
+the temporaries are the rest of the window up to v255, declared clobbered, so
+the compiler's own values stay below or are not live across the blocks.
 """
 import re
 
@@ -65,7 +66,8 @@ def _asm_string(lines):
 SPIN_CAP = 1 << 20  # bounded waits: a flag that never comes ends the wait after this many sleeps
 
 
-def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sync="barrier"):
+def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sync="barrier",
+                    base=None, mul_base=None):
     """C++ text (inside a variant's namespace) of the two asm functions and
     their slot tables, plus allocation statistics.
 
@@ -93,6 +95,10 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
     assert sync in ("barrier", "pairs")
     assert sync == "barrier" or schedule in ("batch", "early")
     assert sync == "pairs" or schedule != "early"
+    # first port register of the accumulator's and the multiplier's blocks
+    # (the roles are separate branches, so their windows may differ)
+    BASE = globals()["BASE"] if base is None else base
+    MUL_BASE = BASE if mul_base is None else mul_base
     ninp, naccp = pad4(nin), pad4(nacc)
     kstride = naccp // 4
     A = list(range(BASE, BASE + naccp))
@@ -237,7 +243,7 @@ static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], cons
 }}
 """
         mul_fn, stats = _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot,
-                                       entry_bytes, st_acc)
+                                       entry_bytes, st_acc, MUL_BASE)
         return accum_fn + mul_fn, stats
 
     carried = [("r", 0, 0)] if schedule == "prefetch" else []
@@ -287,11 +293,12 @@ static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], cons
 }}
 """
     mul_fn, stats = _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot,
-                                   entry_bytes, st_acc)
+                                   entry_bytes, st_acc, MUL_BASE)
     return accum_fn + mul_fn, stats
 
 
-def _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot, entry_bytes, st_acc):
+def _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot, entry_bytes, st_acc,
+                   BASE=BASE):
     """The multiplier role's asm functions (the same for both sync modes)."""
     # ---- multiplier role: product planes go to the P block in slot order
     # (plane b at word prod_slot[b]), so a product is stored with 16-byte
