@@ -88,15 +88,18 @@ def test_conv_null_misaligned_unsupported(hf):
 
 
 def test_split_kernel_availability(hf):
-    """Variants whose netlists do not fit the split kernel's registers refuse
-    SPLIT explicitly and still run FUSED (and AUTO)."""
+    """Every generated variant, the widest extended type included, has both
+    kernel shapes; a format triple with no generated variant is refused for
+    every kernel shape, before anything is launched."""
     wide = dict(in_fmt=(5, 10), acc_fmt=(5, 21), out_fmt=(5, 21))
-    assert hf.conv2d_supported(desc(hf, **wide, algo=hf.ALGO_FUSED))
-    assert hf.conv2d_supported(desc(hf, **wide, algo=hf.ALGO_AUTO))
-    assert not hf.conv2d_supported(desc(hf, **wide, algo=hf.ALGO_SPLIT))
-    d = desc(hf, **wide, algo=hf.ALGO_SPLIT)
-    assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -2
-    assert hf.netlist_ops((5, 10), (5, 21))["mul"] == 0
+    for algo in (hf.ALGO_FUSED, hf.ALGO_AUTO, hf.ALGO_SPLIT):
+        assert hf.conv2d_supported(desc(hf, **wide, algo=algo))
+    assert hf.netlist_ops((5, 10), (5, 21))["mul"] > 0
+    missing = dict(in_fmt=(6, 3), acc_fmt=(6, 4), out_fmt=(6, 4))  # not generated
+    for algo in (hf.ALGO_FUSED, hf.ALGO_AUTO, hf.ALGO_SPLIT):
+        assert not hf.conv2d_supported(desc(hf, **missing, algo=algo))
+        d = desc(hf, **missing, algo=algo)
+        assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -2
     assert hf.conv2d_supported(desc(hf, algo=hf.ALGO_SPLIT))
 
 
