@@ -50,6 +50,24 @@ def test_avgpool_every_variant(v):
 
 
 @pytest.mark.parametrize("rnd", [variants.RNE, variants.RTZ], ids=["rne", "rtz"])
+def test_avgpool_every_pair_of_codes(rnd):
+    """Two positions per image and channel, (5,4) in and out: every pair of
+    codes (x1, x2) -- 2^24 of them, non-canonical specials included -- as one
+    (image, channel), so the adder sees every canonical accumulator value
+    against every code, then the multiply by 1/2. Against the oracle."""
+    hf = need_gpu()
+    N, C = 1 << 12, 1 << 12
+    i = np.arange(N * C, dtype=np.uint64)
+    x = np.stack([i & np.uint64(C - 1), i >> np.uint64(12)], axis=1)  # [pair, position]
+    codes = x.reshape(N, C, 2).transpose(0, 2, 1).reshape(N, 1, 2, C).copy()
+    say(f"avgpool every pair of (5,4) codes rnd={rnd}")
+    got = run_pool(hf, codes, 5, 4, 4, 4, rnd)
+    want = orc.avgpool(codes, 5, 4, 4, 4, rnd=rnd)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{bad.size} mismatches; first at {bad[0]}"
+
+
+@pytest.mark.parametrize("rnd", [variants.RNE, variants.RTZ], ids=["rne", "rtz"])
 def test_avgpool_mobilenet_interface(rnd):
     """The MobileNets shape: batch 16, the last 7 x 7 x 1024 feature map, (5,4)."""
     hf = need_gpu()
