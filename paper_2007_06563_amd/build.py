@@ -158,21 +158,30 @@ def split_asm(wE, wi, wa, rnd, cache):
         acc_c = circuit("accum", (wE, wa), r)[0]
         prod_c = circuit("prod", (wE, wi, wa), r)[0]
         cache[key] = {"text": None, "stats": {"unavailable": "no batch size fits"}}
-        # the largest batch first; for each, the asm register windows from
-        # v96, else from v80, else the accumulator's from v48 (its role keeps
-        # few values of the compiler's; the multiplier's stays at v80)
-        bases = ((96, 96), (80, 80), (48, 80))
-        for K, (base, mul_base) in [(K, b) for K in split_batches(asmgen.pad4(nacc))
-                                    for b in bases]:
-            try:
-                text, stats = asmgen.split_functions(acc_c, prod_c, nin, nacc, K,
-                                                     SPLIT_SLOTS, SPLIT_SCHEDULE, SPLIT_SYNC,
-                                                     base=base, mul_base=mul_base)
-                stats["batch"], stats["base"] = K, [base, mul_base]
-                cache[key] = {"text": text, "stats": stats, "batch": K}
+        # The largest batch that fits; for it, of the asm register windows
+        # below, the one with the fewest bank conflicts (more registers let
+        # the allocator avoid them), the widest compiler share on a tie. The
+        # accumulator's role keeps only a few values of the compiler's, so its
+        # window may start as low as v32; the multiplier's stays at v80 or up.
+        bases = ((96, 96), (80, 80), (48, 80), (32, 80))
+        for K in split_batches(asmgen.pad4(nacc)):
+            best = None
+            for base, mul_base in bases:
+                try:
+                    text, stats = asmgen.split_functions(acc_c, prod_c, nin, nacc, K,
+                                                         SPLIT_SLOTS, SPLIT_SCHEDULE, SPLIT_SYNC,
+                                                         base=base, mul_base=mul_base)
+                except regalloc.AllocError as e:
+                    cache[key] = {"text": None, "stats": {"unavailable": str(e)}}
+                    continue
+                cost = (stats["accum"]["conflicts"] + stats["accum"]["off_bank"]
+                        + stats["mul"]["conflicts"] + stats["mul"]["off_bank"])
+                if best is None or cost < best[0]:
+                    stats["batch"], stats["base"] = K, [base, mul_base]
+                    best = (cost, text, stats)
+            if best is not None:
+                cache[key] = {"text": best[1], "stats": best[2], "batch": K}
                 break
-            except regalloc.AllocError as e:
-                cache[key] = {"text": None, "stats": {"unavailable": str(e)}}
     return cache[key] if cache[key]["text"] is not None else None
 
 
