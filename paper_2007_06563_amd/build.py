@@ -78,7 +78,7 @@ def _build_circuit(kind, key, r):
 
 
 def circuit(kind, key, r):
-    """Optimised circuit of one operator (memoised for this build)."""
+    """Optimised circuit of one operator (memoised per process)."""
     k = (kind, tuple(key), r)
     if k not in _CIRCUITS:
         _CIRCUITS[k] = _build_circuit(kind, key, r)

@@ -329,7 +329,9 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   static_assert(K * NIN <= kConvBlock, "one weight word per multiplier thread");
   static_assert(S * K * 256 * NACCP * 4 <= 144 * 1024, "product ring exceeds the LDS budget");
   static_assert(!V::kPairs || K * NIN <= 64, "pairs: a batch's weights loaded by one wave");
-  __shared__ uint4 pring[S * K * 4 * 64 * kStride];  // [slot][k][wave][lane][kStride]
+  // [slot][k][wave][kStride][lane]: chunk j of the 64 lanes' entries side by
+  // side, so a wave's 16-byte read of one chunk is free of bank conflicts
+  __shared__ uint4 pring[S * K * 4 * kStride * 64];
   // weights: shared ring [slot][k][NINP words] (barrier), or one batch per
   // multiplier wave [wave][k][NINP words] (pairs)
   __shared__ uint4 wring[(V::kPairs ? 4 : 3) * K * NINP / 4];
@@ -354,7 +356,7 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
 
   auto entry = [&](int b, int k) {  // batch b lives in ring slot b % S
     // C-style cast: generic pointer into the LDS address space
-    return (lds_u32*)(pring + ((((size_t)(b % S) * K + k) * 4 + pw) * 64 + lane) * kStride);
+    return (lds_u32*)(pring + (((size_t)(b % S) * K + k) * 4 + pw) * kStride * 64 + lane);
   };
 
   // ---- multiplier waves: weight staging (thread t of the 256 loads word t;
@@ -443,10 +445,11 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
         V::product_step(xw, c, wr + k * NINP, entry(b, k));
         ++c;
       } else {  // tap past the end: product -0 (the sign plane all ones)
-        lds_u32* e = entry(b, k);
+        lds_u32* e = entry(b, k);  // word i of this lane's entry at e[(i/4)*256 + i%4]
 #pragma unroll
-        for (int bb = 0; bb < NACCP; ++bb) e[bb] = 0u;
-        e[V::kProdSlot[NACC - 3]] = 0xFFFFFFFFu;
+        for (int bb = 0; bb < NACCP; ++bb) e[(bb >> 2) * 256 + (bb & 3)] = 0u;
+        const int sg = V::kProdSlot[NACC - 3];
+        e[(sg >> 2) * 256 + (sg & 3)] = 0xFFFFFFFFu;
       }
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // products visible at the barrier

@@ -30,7 +30,7 @@ the compiler's own values stay below or are not live across the blocks.
 """
 import re
 
-from .regalloc import Block, allocate
+from .regalloc import AllocError, Block, allocate
 
 BASE = 96
 TOP = 256
@@ -110,11 +110,17 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
                                     {"acc": (Block(B), "acc")}, pool)
     acc_slot = [r - BASE for r in place["in"]["acc"]]
     prod_slot = [r - P[0][0] for r in place["in"]["p"]]
+    # The ring holds chunk j (16 bytes) of the 64 lanes' entries side by side, so
+    # one ds_read_b128 covers 1 KiB without bank conflicts whatever the entry's
+    # width (a lane-major layout conflicts when the entry is 4 or 8 chunks).
+    chunk_bytes = 64 * 16                # distance between chunks j and j+1
     entry_bytes = 4 * 64 * kstride * 16  # ring distance between batch entries k and k+1
+    if (K - 1) * entry_bytes + (kstride - 1) * chunk_bytes > 0xFFFF:
+        raise AllocError("product ring offsets exceed the 16-bit LDS offset field")
 
     def reads(slot, k):
         return [f"ds_read_b128 v[{P[k][4 * j]}:{P[k][4 * j] + 3}], %[e{slot}] "
-                f"offset:{k * entry_bytes + 16 * j}" for j in range(kstride)]
+                f"offset:{k * entry_bytes + chunk_bytes * j}" for j in range(kstride)]
 
     def netlist(k):
         """Entry k's adder, 8-byte aligned (see ALIGN8)."""
@@ -325,7 +331,8 @@ def _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot, entry_
         out.append("s_nop 4")  # VALU results -> LDS store data
         for j in range(kstride):
             r0 = PB[k % 2][4 * j]
-            out.append(f"ds_write_b128 %[e], v[{r0}:{r0 + 3}] offset:{k * entry_bytes + 16 * j}")
+            out.append(f"ds_write_b128 %[e], v[{r0}:{r0 + 3}] "
+                       f"offset:{k * entry_bytes + 64 * 16 * j}")
         return out
 
     nw, np_ = ninp // 4, kstride

@@ -231,12 +231,20 @@ def test_split_asm_allocation(wE, wi, wa):
 def test_split_asm_text(wE, wi, wa, sync, K):
     """Shape of the generated accumulator loop: one barrier per batch, or
     (pairs) none but a bounded counter wait and a consumed-count store per
-    batch; wait counts within the 4-bit field; registers within v96..v255."""
+    batch; wait counts within the 4-bit field; registers within v96..v255;
+    LDS offsets within the 16-bit field (a ring too deep for it is refused)."""
     import re
     nin, nacc = nbits(wE, wi), nbits(wE, wa)
     acc_c = optimized("accumulate_circuit", wE, wa)
     prod_c = optimized("product_circuit", wE, wi, wa)
+    kstride = asmgen.pad4(nacc) // 4
+    if (K - 1) * 4 * 64 * kstride * 16 + (kstride - 1) * 64 * 16 > 0xFFFF:
+        with pytest.raises(regalloc.AllocError):
+            asmgen.split_functions(acc_c, prod_c, nin, nacc, K, sync=sync)
+        return
     text, _ = asmgen.split_functions(acc_c, prod_c, nin, nacc, K, sync=sync)
+    offsets = [int(x) for x in re.findall(r"offset:(\d+)", text)]
+    assert offsets and max(offsets) <= 0xFFFF
     loop = text[text.index("accum_loop("):text.index("kWSlot")]
     if sync == "barrier":
         assert loop.count("s_barrier") == 2
