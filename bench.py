@@ -182,7 +182,7 @@ def suite(reps):
         del a, b, c, pa, pb, pc, r
     for si, s in enumerate(I.MANTISSA_SWEEP_SHAPES):
         for m in I.MANTISSA_SWEEP_WF:
-            ifm, w = I.conv_inputs(I.MANTISSA_SWEEP, 16 * si + m, s)
+            ifm, w = I.mantissa_sweep_inputs(si, m)
             d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, (5, m),
                              (5, m + 1), (5, m + 1))
             pi = hf.pack(torch.from_numpy(ifm.reshape(-1, s.C)).to(dev), (5, m))
@@ -283,7 +283,7 @@ def sweep(reps):
         ops = hf.netlist_ops((wE, wi), (wE, wa), rnd)
         for batch in (1, 64):
             s = I.mobilenet_layer(batch)
-            ifm, w = I.conv_inputs(I.TYPE_SWEEP, 0, s)
+            ifm, w = I.type_sweep_inputs(batch)
             d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, (wE, wi),
                              (wE, wa), (wE, wo), round=rnd)
             pi = hf.pack(torch.from_numpy(ifm.reshape(-1, s.C)).to(dev), (wE, wi))

@@ -30,8 +30,25 @@
  *    modes the library was generated for (hobflops_conv2d_supported /
  *    hobflops_muladd_supported); other combinations return
  *    HOBFLOPS_EUNSUPPORTED.
- *  - The library keeps no state between calls and is safe to call from
+ *  - Apart from two diagnostics of the split convolution kernel's bounded
+ *    waits (the give-up count and the wait limit, see hobflops_wait_failures),
+ *    the library keeps no state between calls; it is safe to call from
  *    several host threads.
+ *
+ * Where this interface differs from the plain one the paper's problem
+ * statement suggests (format widths, tensor shapes, one accumulation order):
+ *  - hobflops_plane_words returns a status and writes the count through a
+ *    pointer, so that an overflowing size is an error rather than a value;
+ *  - the rounding mode is an argument of hobflops_muladd, hobflops_avgpool and
+ *    hobflops_netlist_ops and a field of hobflops_conv_desc, since the paper
+ *    measures round-toward-zero as well as nearest-even (Sec. 4); its values
+ *    are spelled HOBFLOPS_ROUND_NEAREST_EVEN and HOBFLOPS_ROUND_TOWARD_ZERO;
+ *  - hobflops_conv_desc adds `algo` (the kernel shape) and `ofm_kind` (the
+ *    unpack fused into the last layer's epilogue, Sec. 3.4);
+ *  - hobflops_netlist_ops reports the fused MAC, the multiplier, the
+ *    accumulating adder and the element-wise MAC separately;
+ *  - hobflops_pack_batch, hobflops_avgpool and the *_supported queries are
+ *    additions.
  */
 #ifndef HOBFLOPS_H
 #define HOBFLOPS_H
@@ -200,6 +217,28 @@ int hobflops_avgpool_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, hobflo
  * accumulating add and the final multiply. Any output pointer may be NULL. */
 int hobflops_avgpool_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, hobflops_fmt out_fmt,
                                  int round, int* accum_ops, int* scale_ops);
+
+/* Diagnostics of the split convolution kernel (HOBFLOPS_ALGO_SPLIT). Its
+ * multiplier and accumulator waves hand products over through counters in
+ * LDS; every wait for a counter sleeps at most a bounded number of times
+ * (about 64 clocks each), so that a counter that never came would end the
+ * wait instead of hanging the GPU. A wait that reaches its bound without the
+ * counter is a give-up: that launch's results are invalid, and one give-up is
+ * added to a per-device count.
+ *
+ * hobflops_wait_failures: synchronises the current device, writes its
+ * give-up count (since the library was loaded or last reset) to *count, and
+ * sets it to zero if reset is nonzero. For tests and monitoring, not for hot
+ * loops. Returns HOBFLOPS_OK, HOBFLOPS_EINVAL (count NULL) or HOBFLOPS_EHIP.
+ *
+ * hobflops_set_wait_limit: the bound, in sleeps, for launches made after the
+ * call, process-wide (default 1048576, about 30 ms of sleeping per wait). With
+ * 0 a wait gives up when its first look does not find the counter: tests use
+ * it to check that give-ups are counted. The kernels still finish normally.
+ * hobflops_get_wait_limit returns the current bound. */
+int hobflops_wait_failures(uint32_t* count, int reset);
+int hobflops_set_wait_limit(uint32_t sleeps);
+uint32_t hobflops_get_wait_limit(void);
 
 /* Text for a status code; for HOBFLOPS_EHIP, the last HIP error of this
  * thread. The pointer stays valid until the next call on the same thread. */

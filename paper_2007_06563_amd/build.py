@@ -37,10 +37,73 @@ def nb(wE, wF):
 
 def _gen_sources_digest():
     h = hashlib.sha256()
-    for name in ("circuit.py", "fp.py", "opt.py", "emit.py", "regalloc.py", "asmgen.py"):
+    for name in ("circuit.py", "fp.py", "opt.py", "sim.py", "emit.py", "regalloc.py", "asmgen.py"):
         h.update(open(os.path.join(HERE, "gen", name), "rb").read())
     h.update(open(os.path.abspath(__file__), "rb").read())  # the emission options chosen here
     return h.hexdigest()[:16]
+
+
+def _circuit_sources_digest():
+    """Digest of what the optimised circuits depend on (not their emission)."""
+    h = hashlib.sha256()
+    for name in ("circuit.py", "fp.py", "opt.py", "sim.py"):
+        h.update(open(os.path.join(HERE, "gen", name), "rb").read())
+    h.update(repr(_NONCANONICAL).encode())
+    return h.hexdigest()[:16]
+
+
+def _circuit_to_json(C):
+    return {"name": C.name, "fanins": [list(f) for f in C.fanins], "tts": C.tts,
+            "is_input": C.is_input, "inputs": C.inputs, "outputs": C.outputs,
+            "input_of": [[n, g, b] for n, (g, b) in C.input_of.items()]}
+
+
+def _circuit_from_json(d):
+    from paper_2007_06563_amd.gen.circuit import Circuit
+    C = Circuit(d["name"])
+    C.fanins = [tuple(f) for f in d["fanins"]]
+    C.tts = list(d["tts"])
+    C.is_input = list(d["is_input"])
+    C.inputs = [(g, list(l)) for g, l in d["inputs"]]
+    C.outputs = [(g, list(l)) for g, l in d["outputs"]]
+    C.input_of = {n: (g, b) for n, g, b in d["input_of"]}
+    C.table = {(C.tts[n], C.fanins[n]): n for n in range(1, len(C.fanins)) if not C.is_input[n]}
+    return C
+
+
+def _circuit_key(k):
+    kind, key, r = k
+    return f"{kind}|{','.join(map(str, key))}|{r}"
+
+
+def _load_circuit_cache():
+    """Optimised circuits of earlier builds whose circuit sources are unchanged
+    (the optimisation takes minutes; emission and assembly are redone)."""
+    path = os.path.join(GEN, "circuits.json")
+    if not os.path.exists(path):
+        return
+    try:
+        data = json.load(open(path))
+    except (OSError, ValueError):
+        return
+    if data.get("digest") != _circuit_sources_digest():
+        return
+    for k, (cj, raw) in data["circuits"].items():
+        kind, key, r = k.split("|")
+        t = (kind, tuple(int(v) for v in key.split(",")), r)
+        if t not in _CIRCUITS:
+            _CIRCUITS[t] = (_circuit_from_json(cj), raw)
+
+
+def _save_circuit_cache():
+    path = os.path.join(GEN, "circuits.json")
+    data = {"digest": _circuit_sources_digest(),
+            "circuits": {_circuit_key(k): [_circuit_to_json(C), raw]
+                         for k, (C, raw) in _CIRCUITS.items()}}
+    tmp = path + ".tmp"
+    with open(tmp, "w") as f:
+        json.dump(data, f)
+    os.replace(tmp, path)
 
 
 # Netlists whose results may be non-canonical (they feed only the adder and
@@ -218,7 +281,9 @@ def generate(verbose=True):
             fname, rr = _netlist_name(kind, key, rnd)
             if fname not in cache:
                 needed.append((kind, key, rr))
+    _load_circuit_cache()
     prepare_circuits(needed)
+    _save_circuit_cache()
     for v in variants.CONV_VARIANTS:
         wE, wi, wa, wo, act, rnd = v
         tag = variants.conv_tag(v)
@@ -237,8 +302,8 @@ def generate(verbose=True):
   static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[(NACC + 3) & ~3],
                                                     const lds_u32* e0, const lds_u32* e1,
                                                     const lds_u32* e2, const lds_u32* fl,
-                                                    int nb) {{
-    conv_{tag}::accum_loop(acc, e0, e1, e2, fl, nb);
+                                                    int nb, uint32_t cap, uint32_t& gave) {{
+    conv_{tag}::accum_loop(acc, e0, e1, e2, fl, nb, cap, gave);
   }}
   static __device__ __forceinline__ void product_step(const uint32_t (&xw)[NIN], int c,
                                                       const lds_u32* wrow, lds_u32* entry) {{

@@ -1,11 +1,15 @@
 // C ABI of libhobflops.so (declared in include/hobflops.h): argument checks,
-// variant dispatch and launches. Nothing here computes on the host.
+// variant dispatch and launches. The only value computed on the host is the
+// pooling scale, the code of 1/(H*W) (recip_code); all MAC arithmetic runs in
+// the kernels.
 #include <hip/hip_runtime.h>
 #include <limits.h>
 #include <stdint.h>
 #include <stdio.h>
 #include <string.h>
 
+#include <atomic>
+#include <mutex>
 #include <vector>
 
 #include "hobflops.h"
@@ -17,6 +21,33 @@ using namespace hobflops;
 namespace {
 
 thread_local char g_errbuf[256];
+
+// Give-ups of the split kernel's bounded waits (a diagnostic: each one means
+// that launch's results are invalid). One word per device, in this file's
+// device code; kernels get its address, taken once per device with that
+// device current (the symbol's host-side name is not a device address).
+__device__ uint32_t g_wait_fail_word;
+constexpr int kMaxDevices = 64;
+std::mutex g_wait_mutex;
+uint32_t* g_wait_fail_ptr[kMaxDevices];
+std::atomic<uint32_t> g_spin_cap{kSpinCap};
+
+// The give-up word of the current device (*ptr), or a HIP error.
+hipError_t wait_fail_word(uint32_t** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_wait_mutex);
+  if (!g_wait_fail_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(g_wait_fail_word));
+    if (e != hipSuccess) return e;
+    g_wait_fail_ptr[dev] = static_cast<uint32_t*>(p);
+  }
+  *ptr = g_wait_fail_ptr[dev];
+  return hipSuccess;
+}
 
 int fmt_ok(hobflops_fmt f) {
   return f.wE >= 2 && f.wE <= 8 && f.wF >= 1 && f.wF <= 23 && 3 + f.wE + f.wF <= 32;
@@ -206,6 +237,11 @@ int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
   p.P = p.N * p.OH * p.OW;
   p.ofm_kind = d->ofm_kind;
   p.ofm_vec = ((uintptr_t)ofm & 15u) == 0;
+  p.spin_cap = g_spin_cap.load(std::memory_order_relaxed);
+  {
+    const hipError_t e = wait_fail_word(&p.wait_fail);
+    if (e != hipSuccess) return hip_status(e);
+  }
   int algo = d->algo;
   if (algo == HOBFLOPS_ALGO_AUTO) {
     // one accumulator wave per 64 positions and m-tile; split when they would
@@ -303,6 +339,26 @@ int hobflops_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int round,
   }
   return found ? HOBFLOPS_OK : HOBFLOPS_EUNSUPPORTED;
 }
+
+int hobflops_wait_failures(uint32_t* count, int reset) {
+  if (!count) return HOBFLOPS_EINVAL;
+  uint32_t* word = nullptr;
+  hipError_t e = wait_fail_word(&word);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = hipMemcpy(count, word, sizeof(uint32_t), hipMemcpyDeviceToHost);
+  if (e == hipSuccess && reset) {
+    const uint32_t zero = 0;
+    e = hipMemcpy(word, &zero, sizeof(uint32_t), hipMemcpyHostToDevice);
+  }
+  return hip_status(e);
+}
+
+int hobflops_set_wait_limit(uint32_t sleeps) {
+  g_spin_cap.store(sleeps, std::memory_order_relaxed);
+  return HOBFLOPS_OK;
+}
+
+uint32_t hobflops_get_wait_limit(void) { return g_spin_cap.load(std::memory_order_relaxed); }
 
 const char* hobflops_status_string(int status) {
   switch (status) {

@@ -34,6 +34,11 @@ struct ConvParams {
   int P;   // N * OH * OW output positions
   int ofm_kind;  // kOfmPlanes, kOfmF32 or kOfmCode
   int ofm_vec;   // ofm is 16-byte aligned (value rows may be stored 16 bytes at a time)
+  // Split kernel: every wait of a wave for its partner's counter polls at most
+  // spin_cap times (a sleep of 64 clocks each); a wait that ends there without
+  // the counter adds 1 to *wait_fail (the launch's results are then invalid).
+  uint32_t spin_cap;
+  uint32_t* wait_fail;
 };
 
 // Global average pooling: N images, HW positions each, CG channel words per
@@ -115,8 +120,9 @@ __device__ __forceinline__ void store_ofm(const uint32_t (&out)[NOUT], uint32_t*
 
 constexpr int kConvBlock = 256;  // positions per workgroup: four wave64s
 
-// Bound of every flag wait in the split kernel (sleeps of 64 clocks): a
-// counter that never arrives ends the wait instead of the kernel hanging.
+// Default bound of every counter wait in the split kernel (sleeps of 64
+// clocks): a counter that never arrives ends the wait instead of the kernel
+// hanging, and the give-up is counted (ConvParams::wait_fail).
 constexpr uint32_t kSpinCap = 1u << 20;
 
 // Kernel shapes of the convolution (hobflops_conv_desc.algo).
@@ -480,12 +486,14 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
     // Pairs: accumulator wave pw and multiplier wave 4+pw hand batches over
     // through flags[pw] (made, consumed); LDS operations of one wave complete
     // in order, so a counter written after a wave's stores (and a wait for
-    // them) shows those stores to a reader that reads the counter first. All
-    // waits are bounded by kSpinCap sleeps.
+    // them) shows those stores to a reader that reads the counter first. Every
+    // wait is bounded by p.spin_cap sleeps; a wave whose wait ends there
+    // without its counter counts one give-up in *p.wait_fail.
     // LDS pointers, so that the polls are LDS reads (a generic pointer makes
     // them flat accesses, whose waits also wait for every global load in flight)
     volatile lds_u32* made = (volatile lds_u32*)&flags[pw][0];
     volatile lds_u32* consumed = (volatile lds_u32*)&flags[pw][1];
+    uint32_t gave = 0;  // a wait of this wave gave up (wave-uniform)
     if (mul_role) {
       *made = 0u;
       *consumed = 0u;
@@ -511,9 +519,14 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
         fetch_w(b + 3);
         wreg = wstage;
         if (b >= S) {  // slot b % S held batch b-S: wait until it was added
-          for (uint32_t spin = 0; spin < kSpinCap; ++spin) {
-            if (__builtin_amdgcn_readfirstlane(*consumed) >= (uint32_t)(b - S + 1)) break;
+          uint32_t spin = 0;
+          while (__builtin_amdgcn_readfirstlane(*consumed) < (uint32_t)(b - S + 1)) {
+            if (spin == p.spin_cap) {
+              gave = 1u;
+              break;
+            }
             __builtin_amdgcn_s_sleep(1);
+            ++spin;
           }
         }
         produce(b);  // ends with its stores complete
@@ -527,10 +540,12 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
       }
       if (b < nb) step(b, wa);
       if (b + 1 < nb) step(b + 1, wb);
+      if (gave && lane == 0) atomicAdd(p.wait_fail, 1u);
       return;
     }
     V::accum_loop(acc, entry(0, 0), entry(1, 0), entry(S - 1, 0), (const lds_u32*)&flags[pw][0],
-                  nb);
+                  nb, p.spin_cap, gave);
+    if (gave && lane == 0) atomicAdd(p.wait_fail, 1u);
   } else {
   if (mul_role) {
     __builtin_amdgcn_s_setprio(3);
@@ -551,7 +566,9 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   }
 #pragma unroll
   for (int j = 0; j < S; ++j) __syncthreads();
-  V::accum_loop(acc, entry(0, 0), entry(1, 0), entry(S - 1, 0), nullptr, nb);  // nb barriers
+  uint32_t unused;
+  V::accum_loop(acc, entry(0, 0), entry(1, 0), entry(S - 1, 0), nullptr, nb, 0u,
+                unused);  // nb barriers
   }
   if (!active) return;
   uint32_t planes[NACC], out[NOUT];

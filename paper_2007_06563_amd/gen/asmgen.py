@@ -4,14 +4,16 @@ The two wave roles of the split kernel run their netlists as inline assembly
 with explicit registers chosen by gen.regalloc, so that no VALU instruction
 reads two VGPRs of one bank (see gen/regalloc.py). The functions produced:
 
-* ``accum_loop(acc, e0, e1, e2, fl, nb)``: the whole accumulator role. Batch b
-  (K products) sits in slot b % kSlots of the LDS product ring; its entries
-  are requested with 16-byte loads at immediate offsets from this lane's first
-  entry, on the schedule split_functions is given, and K copies of the adder
-  netlist add them into the accumulator, each waiting for its own entry only.
-  The accumulator ping-pongs between two register sets and is back in the
-  first after the batch (K is even). ``acc`` holds the accumulator planes in
-  register-slot order; kAccSlot[b] is the slot of plane b.
+* ``accum_loop(acc, e0, e1, e2, fl, nb, cap, gave)``: the whole accumulator
+  role. Batch b (K products) sits in slot b % kSlots of the LDS product ring;
+  its entries are requested with 16-byte loads at immediate offsets from this
+  lane's first entry, on the schedule split_functions is given, and K copies
+  of the adder netlist add them into the accumulator, each waiting for its own
+  entry only. The accumulator ping-pongs between two register sets and is
+  back in the first after the batch (K is even). ``acc`` holds the
+  accumulator planes in register-slot order; kAccSlot[b] is the slot of plane
+  b. Each bounded wait polls at most ``cap`` times; ``gave`` reports a wait
+  that gave up.
 * ``product_batch(xw, c, wrow, entry)``: the K products of one batch whose
   taps c .. c+K-1 lie in one IFM channel word: all K weight rows are requested
   from the LDS weight ring first (plane b in word kWSlot[b]); per product, bit
@@ -63,9 +65,6 @@ def _asm_string(lines):
     return "\n".join(f'      "{ln}\\n"' for ln in lines)
 
 
-SPIN_CAP = 1 << 20  # bounded waits: a flag that never comes ends the wait after this many sleeps
-
-
 def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sync="barrier",
                     base=None, mul_base=None):
     """C++ text (inside a variant's namespace) of the two asm functions and
@@ -84,7 +83,9 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
     the batch's products and uses them if the counter shows the batch (LDS
     operations of a wave complete in order, and the multiplier writes the
     counter after its products); else it polls the counter alone, with a
-    sleep between reads, at most SPIN_CAP times, and reads the products again.
+    sleep between reads, at most `cap` times (a run-time argument), and reads
+    the products again; a wait that used up its polls without seeing the
+    batch sets `gave` (the caller records it: the results are then invalid).
     After the batch it writes the consumed count. With schedule "early" the
     consumed count is written as soon as the last entry's products are in
     registers, and the counter and entry 0 of the next batch are requested
@@ -157,7 +158,7 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
         """One batch handed over through the counters (see sync). The
         counter is read together with the batch's products; if it does not
         show the batch yet, the products are dropped and only the counter is
-        read again, after a sleep, until it does (at most SPIN_CAP times);
+        read again, after a sleep, until it does (at most `cap` times);
         then the products are read once more."""
         n_reads = K * kstride
         early = schedule == "early"
@@ -180,6 +181,8 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
                 "s_waitcnt lgkmcnt(0)",             # batch not made yet: drop the loads
                 "s_mov_b32 %[spin], 0",
                 f"L%=_poll{slot}:",
+                "s_cmp_ge_u32 %[spin], %[cap]",     # the wait's sleeps used up: give up
+                f"s_cbranch_scc1 L%=_giveup{slot}",
                 "s_sleep 1",
                 f"ds_read_b32 v{VF}, %[fl]",
                 "s_waitcnt lgkmcnt(0)",
@@ -187,9 +190,10 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
                 "s_nop 4",
                 "s_add_u32 %[spin], %[spin], 1",
                 "s_cmp_ge_u32 %[t], %[b1]",
-                f"s_cbranch_scc1 L%=_again{slot}",
-                f"s_cmp_lt_u32 %[spin], {SPIN_CAP}",
-                f"s_cbranch_scc1 L%=_poll{slot}",
+                f"s_cbranch_scc0 L%=_poll{slot}",
+                f"s_branch L%=_again{slot}",
+                f"L%=_giveup{slot}:",
+                "s_mov_b32 %[gave], 1",             # recorded by the caller
                 f"L%=_again{slot}:"]
         release = [f"v_mov_b32 v{VB}, %[b1]",
                    "s_nop 4",                      # VALU result -> LDS store data
@@ -216,7 +220,8 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
         return out
 
     if sync == "pairs":
-        body = ["s_waitcnt lgkmcnt(0)", "s_mov_b32 %[n], %[nb]", "s_mov_b32 %[b1], 1"]
+        body = ["s_waitcnt lgkmcnt(0)", "s_mov_b32 %[n], %[nb]", "s_mov_b32 %[b1], 1",
+                "s_mov_b32 %[gave], 0"]
         if schedule == "early":
             body += [f"ds_read_b32 v{VF}, %[fl]"] + reads(0, 0)
         body += ["L%=_loop:"]
@@ -236,15 +241,18 @@ static constexpr bool kPairs = true;
 // The accumulator role: nb batches of K products from the LDS ring of kSlots
 // slots (this lane's first entry of slot s at e_s, batch b in slot b % kSlots),
 // handed over by the multiplier wave through the counters at fl (made at fl,
-// consumed at fl + 4); acc holds the planes in register-slot order.
+// consumed at fl + 4); acc holds the planes in register-slot order. Each wait
+// for a batch sleeps at most cap times; gave is set when one gave up.
 static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], const lds_u32* e0,
                                                   const lds_u32* e1, const lds_u32* e2,
-                                                  const lds_u32* fl, int nb) {{
+                                                  const lds_u32* fl, int nb, uint32_t cap,
+                                                  uint32_t& gave) {{
   uint32_t n, b1, spin, t;
   asm volatile(
 {_asm_string(body)}
-      : {state}, [n] "=&s"(n), [b1] "=&s"(b1), [spin] "=&s"(spin), [t] "=&s"(t)
-      : [e0] "v"(e0), [e1] "v"(e1), [e2] "v"(e2), [fl] "v"(fl), [nb] "s"(nb)
+      : {state}, [n] "=&s"(n), [b1] "=&s"(b1), [spin] "=&s"(spin), [t] "=&s"(t),
+        [gave] "=&s"(gave)
+      : [e0] "v"(e0), [e1] "v"(e1), [e2] "v"(e2), [fl] "v"(fl), [nb] "s"(nb), [cap] "s"(cap)
       : {clob}, "scc", "memory");
 }}
 """
@@ -286,11 +294,13 @@ static constexpr bool kPairs = false;
 // The accumulator role: nb batches of K products from the LDS ring of kSlots
 // slots (this lane's first entry of slot s at e_s, batch b in slot b % kSlots),
 // one barrier after each batch; acc holds the planes in register-slot order
-// (fl, the pairs' counters, is not used).
+// (fl, cap and gave, the pairs' counters and bounded waits, are not used).
 static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], const lds_u32* e0,
                                                   const lds_u32* e1, const lds_u32* e2,
-                                                  const lds_u32* fl, int nb) {{
+                                                  const lds_u32* fl, int nb, uint32_t cap,
+                                                  uint32_t& gave) {{
   uint32_t n;
+  gave = 0;
   asm volatile(
 {_asm_string(body)}
       : {state}, [n] "=&s"(n)

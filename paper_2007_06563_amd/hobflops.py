@@ -52,7 +52,8 @@ EXPORTS = ("hobflops_plane_words", "hobflops_pack", "hobflops_pack_batch", "hobf
            "hobflops_conv2d",
            "hobflops_conv2d_supported", "hobflops_muladd", "hobflops_muladd_supported",
            "hobflops_netlist_ops", "hobflops_avgpool", "hobflops_avgpool_supported",
-           "hobflops_avgpool_netlist_ops", "hobflops_status_string")
+           "hobflops_avgpool_netlist_ops", "hobflops_wait_failures", "hobflops_set_wait_limit",
+           "hobflops_get_wait_limit", "hobflops_status_string")
 
 
 def lib():
@@ -76,10 +77,14 @@ def lib():
         L.hobflops_avgpool.argtypes = [vp, vp, ci, ci, ci, ci, Fmt, Fmt, Fmt, ci, vp]
         L.hobflops_avgpool_supported.argtypes = [Fmt, Fmt, Fmt, ci]
         L.hobflops_avgpool_netlist_ops.argtypes = [Fmt, Fmt, Fmt, ci] + [ctypes.POINTER(ci)] * 2
+        L.hobflops_wait_failures.argtypes = [ctypes.POINTER(ctypes.c_uint32), ci]
+        L.hobflops_set_wait_limit.argtypes = [ctypes.c_uint32]
+        L.hobflops_get_wait_limit.argtypes = []
         L.hobflops_status_string.argtypes = [ci]
         L.hobflops_status_string.restype = ctypes.c_char_p
         for name in EXPORTS[:-1]:
             getattr(L, name).restype = ci
+        L.hobflops_get_wait_limit.restype = ctypes.c_uint32
         _lib = L
     return _lib
 
@@ -283,3 +288,22 @@ def avgpool_netlist_ops(in_fmt, acc_fmt, out_fmt, round=ROUND_NEAREST_EVEN):
     if rc != 0:
         raise HobflopsError(rc, lib().hobflops_status_string(rc).decode())
     return dict(zip(("accum", "scale"), (x.value for x in v)))
+
+
+def wait_failures(reset=True):
+    """Give-ups of the split kernel's bounded waits on the current device since
+    the last reset (synchronises the device); nonzero means some launch's
+    results are invalid."""
+    n = ctypes.c_uint32()
+    _check(lib().hobflops_wait_failures(ctypes.byref(n), 1 if reset else 0))
+    return n.value
+
+
+def set_wait_limit(sleeps):
+    """Bound, in sleeps, of every counter wait in later split-kernel launches
+    (process-wide; 0 gives up at the first look that misses)."""
+    _check(lib().hobflops_set_wait_limit(int(sleeps)))
+
+
+def get_wait_limit():
+    return int(lib().hobflops_get_wait_limit())

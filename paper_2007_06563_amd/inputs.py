@@ -152,6 +152,19 @@ def resnet_conv_inputs():
     return conv_inputs(RESNET_CONV, 0, RESNET_CONV_SHAPE, w_std=0.05)
 
 
+def mantissa_sweep_inputs(shape_index, wF):
+    """The mantissa sweep's layers take the ResNet layer's value distributions:
+    ReLU-like IFM, weights N(0, 0.05)."""
+    return conv_inputs(MANTISSA_SWEEP, 16 * shape_index + wF, MANTISSA_SWEEP_SHAPES[shape_index],
+                       w_std=0.05)
+
+
+def type_sweep_inputs(batch):
+    """Inputs of the MobileNets-shaped layer of the type sweep: ReLU-like IFM,
+    weights N(0, sqrt(2/fan_in)) (an initialised layer of 4,608 taps)."""
+    return conv_inputs(TYPE_SWEEP, 0, mobilenet_layer(batch))
+
+
 def random_codes(seed, shape, nbits):
     """Raw codes with every one of the low nbits drawn at random (this includes
     non-canonical special values) -- for exercising code inputs."""

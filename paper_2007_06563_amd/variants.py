@@ -7,7 +7,9 @@ Convolution variants are (wE, wF_in, wF_acc, wF_out, act, round):
     "extended" type (2wF+1 bits: the product is exact), each rounding to
     nearest even and toward zero (Sec. 4);
   * the ReLU + format-change epilogues of a stack of layers whose inputs
-    alternate between (5,3) and (5,5).
+    alternate between (5,3) and (5,5);
+  * HOBFLOPS9 accumulating in its own input format, (5,3) -> (5,3): the
+    small convolution read literally, "accumulate in the same format".
 Element-wise MAC variants are (wE, wF_in, wF_acc, round).
 Global average pooling variants are (wE, wF_in, wF_acc, wF_out, round): the
 output format of every "single" convolution variant of the sweep pooled in
@@ -21,6 +23,7 @@ CONV_VARIANTS = (
     [(wE, m, m + 1, m + 1, 0, r) for r in (RNE, RTZ) for wE, m in SWEEP_TYPES]
     + [(wE, m, 2 * m + 1, 2 * m + 1, 0, r) for r in (RNE, RTZ) for wE, m in SWEEP_TYPES]
     + [(5, 3, 4, 5, 1, RNE), (5, 5, 6, 3, 1, RNE), (5, 3, 4, 4, 1, RNE)]
+    + [(5, 3, 3, 3, 0, r) for r in (RNE, RTZ)]
 )
 
 MULADD_VARIANTS = [(wE, wi, wa, r) for r in (RNE, RTZ) for wE, wi, wa in

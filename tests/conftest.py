@@ -14,3 +14,21 @@ if TESTS not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU")
     config.addinivalue_line("markers", "slow: long-running CPU test")
+
+
+@pytest.fixture(autouse=True)
+def _split_kernel_waits_never_give_up(request):
+    """After every GPU test: no bounded wait of the split convolution kernel
+    gave up (a give-up would mean some launch's results are invalid even if
+    the test's own checks passed). The count is reset for the next test."""
+    yield
+    if request.node.get_closest_marker("gpu") is None:
+        return
+    import torch
+    if not torch.cuda.is_available():
+        return
+    from paper_2007_06563_amd import hobflops as hf
+    if hf._lib is None:
+        return
+    n = hf.wait_failures(reset=True)
+    assert n == 0, f"{n} bounded waits of the split kernel gave up during this test"

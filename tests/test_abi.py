@@ -226,3 +226,19 @@ def test_avgpool_argument_checks(hf):
     assert not hf.avgpool_supported((5, 4), (5, 5), (5, 5))
     ops = hf.avgpool_netlist_ops((5, 4), (5, 4), (5, 4))
     assert ops["accum"] == hf.netlist_ops((5, 3), (5, 4))["accum"] and ops["scale"] > 0
+
+
+def test_wait_limit_and_failure_query_arguments(hf):
+    """The split kernel's wait bound is a process-wide setting read at launch;
+    the give-up query refuses a NULL output before touching the device."""
+    L = hf.lib()
+    default = hf.get_wait_limit()
+    assert default == 1 << 20
+    try:
+        hf.set_wait_limit(0)
+        assert hf.get_wait_limit() == 0
+        hf.set_wait_limit(12345)
+        assert L.hobflops_get_wait_limit() == 12345
+    finally:
+        hf.set_wait_limit(default)
+    assert L.hobflops_wait_failures(None, 0) == -1

@@ -370,30 +370,6 @@ def test_conv_tap_counts_not_multiple_of_batch(algo):
         assert np.array_equal(got, orc.conv2d(qi, qw, 1, pad, 5, 3, 4, 4))
 
 
-def test_resnet_conv_layer_sampled():
-    """8x56x56x64 -> 64 kernels 3x3 in (5,3)/(5,4): every output computed on
-    the GPU, a sample (all four borders of every image plus random interior
-    points, every kernel) recomputed by the oracle."""
-    hf = need_gpu()
-    s = I.RESNET_CONV_SHAPE
-    ifm, w = I.resnet_conv_inputs()
-    qi, qw = orc.quantize_f32(ifm, 5, 3), orc.quantize_f32(w, 5, 3)
-    say("conv resnet layer 8x56x56x64->64")
-    got = run_conv(hf, qi, qw, 1, 1, 5, 3, 4, 4, 0)
-    g = np.random.default_rng(0)
-    pts = []
-    for n in range(s.N):
-        for t in range(s.OW):
-            for oy, ox in ((0, t), (s.OH - 1, t), (t, 0), (t, s.OW - 1)):
-                pts.append((n, oy, ox, g.integers(0, s.M)))
-    for _ in range(4096):
-        pts.append((g.integers(0, s.N), g.integers(0, s.OH), g.integers(0, s.OW), g.integers(0, s.M)))
-    pts = np.array(pts, np.int64)
-    want = orc.conv2d_points(qi, qw, pts, 1, 1, 5, 3, 4, 4)
-    gotp = got[pts[:, 0], pts[:, 1], pts[:, 2], pts[:, 3]]
-    assert np.array_equal(gotp, want)
-
-
 @pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
 @pytest.mark.parametrize("M", [64, 40, 37])
 def test_conv_fused_unpack(algo, M):

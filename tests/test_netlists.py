@@ -230,8 +230,8 @@ def test_split_asm_allocation(wE, wi, wa):
 @pytest.mark.parametrize("wE,wi,wa", [(5, 3, 4), (5, 4, 5)])
 def test_split_asm_text(wE, wi, wa, sync, K):
     """Shape of the generated accumulator loop: one barrier per batch, or
-    (pairs) none but a bounded counter wait and a consumed-count store per
-    batch; wait counts within the 4-bit field; registers within v96..v255;
+    (pairs) none but a counter wait bounded by the run-time cap (a give-up
+    reported) and a consumed-count store per batch; wait counts within the 4-bit field; registers within v96..v255;
     LDS offsets within the 16-bit field (a ring too deep for it is refused)."""
     import re
     nin, nacc = nbits(wE, wi), nbits(wE, wa)
@@ -251,7 +251,10 @@ def test_split_asm_text(wE, wi, wa, sync, K):
     else:
         assert "s_barrier" not in loop
         assert loop.count("s_sleep") == 2 and loop.count("v_readfirstlane_b32") == 4
-        assert loop.count("ds_write_b32") == 2 and f"{asmgen.SPIN_CAP}" in loop
+        assert loop.count("ds_write_b32") == 2
+        # every wait is bounded by the run-time cap, and a give-up is reported
+        assert loop.count("s_cmp_ge_u32 %[spin], %[cap]") == 2
+        assert loop.count("s_mov_b32 %[gave], 1") == 2 and "s_mov_b32 %[gave], 0" in loop
     waits = [int(x) for x in re.findall(r"lgkmcnt\((\d+)\)", text)]
     assert waits and max(waits) <= 15
     regs = [int(x) for x in re.findall(r"\bv(\d+)\b", text)]
