@@ -38,11 +38,15 @@ from paper_2007_06563_amd import inputs as I     # noqa: E402
 N_CU, LANES_PER_CU_CLK, CLOCK_HZ = 256, 128, 2.4e9
 PEAK_LANE_OPS = N_CU * LANES_PER_CU_CLK * CLOCK_HZ   # 7.86e13 32-bit VALU ops/s
 N_SIMD = N_CU * 4
-SINGLE_WAVE_SHARE = 0.5
 HBM_PEAK = 8.0e12
-# clocks per instruction of one wave running a netlist alone (measured on
-# MI355X over long 8-byte-aligned straight-line runs)
-ISSUE_CLOCKS = 4.04
+# clocks per instruction of one wave with a SIMD to itself (measured on MI355X
+# with the split kernel's accumulator loop alone in the kernel, shader-clock
+# stamps around the loop: 4.44; a synthetic stream of 8-byte v_bitop3_b32
+# measures 4.54 per instruction including its loop branch), and of a SIMD
+# shared by two or more waves of bank-conflict-free bitwise instructions
+# (2.24-2.36: the peak assumes 2)
+ISSUE_CLOCKS = 4.44
+SIMD_CLOCKS = 2.24
 
 IN_FMT, ACC_FMT, OUT_FMT = (5, 3), (5, 4), (5, 4)
 
@@ -132,6 +136,31 @@ def _conv_ops(d):
     return algo, (ops["mul"] + ops["accum"] if algo == hf.ALGO_SPLIT else ops["mac"])
 
 
+def issue_ceiling(d, algo):
+    """The share of the VALU peak a convolution launch can reach, from its
+    structure at the nominal clock: every output is one chain of taps in a
+    fixed order, and a wave issues at most one instruction per ISSUE_CLOCKS.
+    Split kernel: one accumulator wave per chain set, on a SIMD of its own, so
+    the time is at least taps x adder instructions x ISSUE_CLOCKS. Fused
+    kernel: a wave's taps x MAC instructions x ISSUE_CLOCKS, or its SIMD's
+    share of all waves x SIMD_CLOCKS per instruction when several share one
+    (workgroups of four waves spread over a CU's four SIMDs)."""
+    OH, OW = hf.conv_out_hw(d)
+    P, taps = d.N * OH * OW, d.KH * d.KW * d.C
+    chain_waves = ((P + 63) // 64) * ((d.M + 31) // 32)
+    ops = hf.netlist_ops((d.in_fmt.wE, d.in_fmt.wF), (d.acc_fmt.wE, d.acc_fmt.wF), d.round)
+    if algo == hf.ALGO_SPLIT:
+        G, clocks = ops["mul"] + ops["accum"], taps * ops["accum"] * ISSUE_CLOCKS
+        if chain_waves > N_SIMD:  # more chain sets than SIMDs: some run one after another
+            clocks *= -(-chain_waves // N_SIMD)
+    else:
+        G = ops["mac"]
+        wgs_per_cu = -(-((P + 255) // 256) * ((d.M + 31) // 32) // N_CU)
+        clocks = taps * G * max(ISSUE_CLOCKS, wgs_per_cu * SIMD_CLOCKS)
+    lane_ops = P * d.M * taps / 32.0 * G
+    return min(1.0, lane_ops / (clocks / CLOCK_HZ) / PEAK_LANE_OPS)
+
+
 def pack_bench(reps):
     """Pack and unpack alone, on the element-wise workload's first operand
     (2^24 float32 values, (5,3)): one JSON line each, GB/s against 8 TB/s.
@@ -156,13 +185,33 @@ def pack_bench(reps):
                          "unit": "GB/s", "frac": nbytes / (ms * 1e-3) / HBM_PEAK}}), flush=True)
 
 
-def suite(reps):
+def suite(reps, only=None):
     """One JSON line per further workload: the element-wise sweep and
     pack/unpack against HBM, the mantissa sweep and the 13-layer stack
-    against the VALU peak. Inputs resident in HBM; kernels only."""
+    against the VALU peak. Inputs resident in HBM; kernels only. With `only`,
+    just the workloads whose label contains that text (for profiling one)."""
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
+
+    def want(label):
+        return only is None or only in label
+
+    if want("device copy"):
+        # what a plain device-to-device copy reaches on this GPU: the practical
+        # HBM ceiling the HBM-bound kernels are compared with
+        a = torch.empty(1 << 26, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        ms = _time(lambda: b.copy_(a), reps, stream)
+        print(json.dumps({
+            "workload": "device copy 256 MiB (reference for the HBM-bound kernels)",
+            "kernel": "torch copy_", "ms": ms,
+            "roofline": {"bound": "hbm", "achieved": 2 * a.numel() * 4 / (ms * 1e-3) / 1e9,
+                         "peak": 8000.0, "unit": "GB/s",
+                         "frac": 2 * a.numel() * 4 / (ms * 1e-3) / HBM_PEAK}}), flush=True)
+        del a, b
     for idx, (wE, wF) in enumerate(I.FMA_FORMATS):
+        if not want(f"element-wise a*b+c, 2^24 triples, ({wE},{wF}) -> ({wE},{wF + 1})"):
+            continue
         a, b, c = (torch.from_numpy(t.reshape(1, -1)).to(dev) for t in I.fma_operands(idx))
         n = a.numel()
         f, fa = (wE, wF), (wE, wF + 1)
@@ -182,6 +231,9 @@ def suite(reps):
         del a, b, c, pa, pb, pc, r
     for si, s in enumerate(I.MANTISSA_SWEEP_SHAPES):
         for m in I.MANTISSA_SWEEP_WF:
+            label = f"conv {s.N}x{s.H}x{s.W}x{s.C} -> {s.M} 3x3, (5,{m}) -> (5,{m + 1})"
+            if not want(label):
+                continue
             ifm, w = I.mantissa_sweep_inputs(si, m)
             d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, (5, m),
                              (5, m + 1), (5, m + 1))
@@ -192,14 +244,23 @@ def suite(reps):
             algo, G = _conv_ops(d)
             lane_ops = s.macs / 32.0 * G
             print(json.dumps({
-                "workload": f"conv {s.N}x{s.H}x{s.W}x{s.C} -> {s.M} 3x3, (5,{m}) -> (5,{m + 1})",
+                "workload": label,
                 "kernel": "split" if algo == hf.ALGO_SPLIT else "fused", "ms": ms,
                 "gmacs": s.macs / (ms * 1e-3) / 1e9, "ops_per_mac_word": G,
                 "roofline": {"bound": "alu", "achieved": lane_ops / (ms * 1e-3) / 1e12,
                              "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
-                             "frac": lane_ops / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
+                             "frac": lane_ops / (ms * 1e-3) / PEAK_LANE_OPS,
+                             "issue_ceiling": issue_ceiling(d, algo)}}), flush=True)
     shapes = I.resnet_stack_shapes(16)
     fmts = I.resnet_stack_formats(len(shapes))
+    stack_labels = [f"stack layer {li + 1}: {s.N}x{s.H}x{s.W}x{s.C} -> {s.M} {s.KH}x{s.KW} "
+                    f"s{s.stride}, (5,{fmts[li][0]}) -> (5,{fmts[li][1]}) -> (5,{fmts[li][2]}) relu"
+                    for li, s in enumerate(shapes)]
+    stack_label = "13-layer stack, batch 16, 56x56x64 input, planes resident between layers"
+    pool_labels = ["global average pooling, 13-layer stack output: 16x7x7x512, (5,4)",
+                   "global average pooling, MobileNets interface: 16x7x7x1024, (5,4)"]
+    if not any(want(x) for x in stack_labels + [stack_label] + pool_labels):
+        return
     ifm0, _ = I.conv_inputs(I.RESNET_STACK, 0, shapes[0])
     x0 = hf.pack(torch.from_numpy(ifm0.reshape(-1, shapes[0].C)).to(dev), (5, fmts[0][0]))
     layers = []
@@ -214,39 +275,44 @@ def suite(reps):
         acts.append(hf.conv2d(acts[-1], pw, d))
     total_ms, total_macs, total_ops = 0.0, 0, 0.0
     for li, (s, d, pw) in enumerate(layers):
-        src, dst = acts[li], acts[li + 1]
-        ms = _time(lambda: hf.conv2d(src, pw, d, out=dst), reps, stream)
         algo, G = _conv_ops(d)
-        total_ms += ms
         total_macs += s.macs
         total_ops += s.macs / 32.0 * G
+        if not want(stack_labels[li]):
+            continue
+        src, dst = acts[li], acts[li + 1]
+        ms = _time(lambda: hf.conv2d(src, pw, d, out=dst), reps, stream)
+        total_ms += ms
         print(json.dumps({
-            "workload": f"stack layer {li + 1}: {s.N}x{s.H}x{s.W}x{s.C} -> {s.M} {s.KH}x{s.KW} "
-                        f"s{s.stride}, (5,{fmts[li][0]}) -> (5,{fmts[li][1]}) -> (5,{fmts[li][2]}) "
-                        "relu",
+            "workload": stack_labels[li],
             "kernel": "split" if algo == hf.ALGO_SPLIT else "fused", "ms": ms,
             "gmacs": s.macs / (ms * 1e-3) / 1e9, "ops_per_mac_word": G,
             "roofline": {"bound": "alu", "achieved": s.macs / 32.0 * G / (ms * 1e-3) / 1e12,
                          "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
-                         "frac": s.macs / 32.0 * G / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
+                         "frac": s.macs / 32.0 * G / (ms * 1e-3) / PEAK_LANE_OPS,
+                         "issue_ceiling": issue_ceiling(d, algo)}}), flush=True)
+    if not want(stack_label) and not any(want(x) for x in pool_labels):
+        return
 
     def whole():
         for li, (s, d, pw) in enumerate(layers):
             hf.conv2d(acts[li], pw, d, out=acts[li + 1])
-    ms = _time(whole, max(1, reps // 4), stream)
-    print(json.dumps({
-        "workload": "13-layer stack, batch 16, 56x56x64 input, planes resident between layers",
-        "ms": ms, "sum_of_layers_ms": total_ms, "gmacs": total_macs / (ms * 1e-3) / 1e9,
-        "roofline": {"bound": "alu", "achieved": total_ops / (ms * 1e-3) / 1e12,
-                     "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
-                     "frac": total_ops / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
+    if want(stack_label):
+        ms = _time(whole, max(1, reps // 4), stream)
+        print(json.dumps({
+            "workload": stack_label,
+            "ms": ms, "sum_of_layers_ms": total_ms, "gmacs": total_macs / (ms * 1e-3) / 1e9,
+            "roofline": {"bound": "alu", "achieved": total_ops / (ms * 1e-3) / 1e12,
+                         "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
+                         "frac": total_ops / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
     # global average pooling in the packed format: the stack's last 7 x 7 x 512
     # map, and the MobileNets interface shape 7 x 7 x 1024, both batch 16
     s_last = shapes[-1]
     x1024 = hf.pack(torch.from_numpy(np.random.default_rng(5).normal(
         size=(16 * 49, 1024)).astype(np.float32)).to(dev), (5, 4))
-    for name, src, C in (("13-layer stack output", acts[-1], s_last.M),
-                         ("MobileNets interface", x1024, 1024)):
+    for label, src, C in ((pool_labels[0], acts[-1], s_last.M), (pool_labels[1], x1024, 1024)):
+        if not want(label):
+            continue
         N, H, W = 16, 7, 7
         f = (5, 4)
         o = hf.avgpool(src, N, H, W, C, f, f, f)
@@ -256,7 +322,7 @@ def suite(reps):
         lane_ops = words * (H * W * ops["accum"] + ops["scale"])
         chain_us = H * W * ops["accum"] * ISSUE_CLOCKS / 2.3e3
         print(json.dumps({
-            "workload": f"global average pooling, {name}: {N}x{H}x{W}x{C}, (5,4)",
+            "workload": label,
             "kernel": "avgpool_kernel", "ms": ms, "g_adds": N * C * H * W / (ms * 1e-3) / 1e9,
             "chain_bound_us": chain_us, "lanes": words,
             "roofline": {"bound": "alu", "achieved": lane_ops / (ms * 1e-3) / 1e12,
@@ -303,7 +369,8 @@ def sweep(reps):
                 "gmacs": s.macs / (ms * 1e-3) / 1e9,
                 "roofline": {"bound": "alu", "achieved": lane_ops / (ms * 1e-3) / 1e12,
                              "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
-                             "frac": lane_ops / (ms * 1e-3) / PEAK_LANE_OPS}}), flush=True)
+                             "frac": lane_ops / (ms * 1e-3) / PEAK_LANE_OPS,
+                             "issue_ceiling": issue_ceiling(d, algo)}}), flush=True)
 
 
 def main():
@@ -328,6 +395,8 @@ def main():
     ap.add_argument("--suite", action="store_true",
                     help="instead of the one-line benchmark: one JSON line per further workload "
                          "(element-wise sweep, mantissa sweep, 13-layer stack)")
+    ap.add_argument("--only", default=None,
+                    help="with --suite: only the workloads whose label contains this text")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the layer shards "
@@ -337,7 +406,7 @@ def main():
     torch.cuda.init()
     dev = torch.device("cuda:0")
     if args.suite:
-        suite(args.steps)
+        suite(args.steps, args.only)
         return
     if args.pack:
         pack_bench(args.steps)
@@ -415,15 +484,7 @@ def main():
     G = ops["mul"] + ops["accum"] if algo == hf.ALGO_SPLIT else ops["mac"]
     lane_ops = macs / 32.0 * G          # 32 MACs per 32-bit word operation
     achieved = lane_ops / (conv_ms * 1e-3)
-    waves = ((P + 63) // 64) * ((s.M + 31) // 32)
-    if algo == hf.ALGO_SPLIT:
-        # each accumulator wave has a SIMD of its own; its chain of taps x
-        # adder instructions, one every ISSUE_CLOCKS at the nominal clock,
-        # bounds the kernel's time and hence its share of the peak
-        chain_s = s.KH * s.KW * s.C * ops["accum"] * ISSUE_CLOCKS / CLOCK_HZ
-        issue_ceiling = min(1.0, lane_ops / chain_s / PEAK_LANE_OPS)
-    else:
-        issue_ceiling = min(1.0, waves * SINGLE_WAVE_SHARE / N_SIMD)
+    ceiling = issue_ceiling(d, algo)
     pack_bytes = (s.N * s.H * s.W * s.C + s.KH * s.KW * s.C * s.M) * 4 + \
         (p_ifm.numel() + p_w.numel()) * 4
     d_codes = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, IN_FMT, ACC_FMT,
@@ -456,7 +517,7 @@ def main():
                      "kernel": "conv2d_split_kernel" if algo == hf.ALGO_SPLIT else "conv2d_kernel",
                      "ops_per_mac_word": G,
                      "kernel_ms": conv_ms,
-                     "issue_ceiling": issue_ceiling},
+                     "issue_ceiling": ceiling},
         "pct_valu_peak": 100.0 * achieved / PEAK_LANE_OPS,
         "conv_gmacs": macs / (conv_ms * 1e-3) / 1e9,
         "pack_ms": pack_ms,

@@ -40,37 +40,54 @@ __device__ __forceinline__ uint32_t quantize_bits(uint32_t bits, int wE, int wF)
   return code;
 }
 
-// The same code as quantize_bits for wE <= 7, in fewer instructions. Such a
-// format's smallest normal is 2^-63 or larger, so every float32 subnormal (and
-// any value the add below might flush) lies below the range. For |x| in
-// [2^u, 2^(u+1)), C = 2^(u + 23 - wF) has the ulp 2^(u - wF) in its binade and
-// |x| + C stays in that binade, so the float32 add rounds |x| to wF fraction
-// bits, ties to even (the multiple index of C is even), and subtracting C
-// again is exact; a round-up into the next binade shows in the result's
-// exponent. The exponent field then moves by the bias difference, and the
-// sign of t tells an underflow. |x| is clamped to 2^100, which every such
-// format overflows, so that C stays finite; NaN is tested on the input.
+// The same code as quantize_bits for wE <= 7 and wF <= 22, in fewer
+// instructions. Such a format's smallest normal is 2^-63 or larger, so every
+// float32 subnormal (and any value the add below might flush) lies below the
+// range. For |x| in [2^u, 2^(u+1)), C = 2^(u + 23 - wF) has the ulp
+// 2^(u - wF) in its binade and |x| + C stays in that binade, so the float32
+// add rounds |x| to wF fraction bits, ties to even (the multiple index of C
+// is even), and subtracting C again is exact; a round-up into the next
+// binade shows in the result's exponent. The exponent field then moves by
+// the bias difference, and the sign of t tells an underflow. |x| is clamped
+// to 2^100, which every such format overflows, so that C stays finite; NaN is
+// tested on the input. The three special cases are selected with all-ones
+// masks (arithmetic shifts of a difference's sign), each in one v_bitop3_b32
+// (truth table 0xCA: mask ? a : b).
 __device__ __forceinline__ uint32_t quantize_narrow(uint32_t bits, int wE, int wF) {
   const uint32_t a = bits & 0x7FFFFFFFu;
   const uint32_t ac = min(a, 0x71800000u);
   const int k = 23 - wF;
   const float C = __uint_as_float((ac & 0x7F800000u) + ((uint32_t)k << 23));
-  // wF = 23 keeps every bit: nothing to round
-  const float r = k > 0 ? __fsub_rn(__fadd_rn(__uint_as_float(ac), C), C) : __uint_as_float(ac);
+  const float r = __fsub_rn(__fadd_rn(__uint_as_float(ac), C), C);
   const int bias = (1 << (wE - 1)) - 1;
   const int t = (int)(__float_as_uint(r) >> k) - ((127 - bias) << wF);
   const int sh_x = wF + wE + 1;
   const uint32_t sgn = (bits >> 31) << (wF + wE);
-  // the cases are selected with all-ones masks (arithmetic shifts of a
-  // difference's sign): as selects, the compiler turns some into branches
   const uint32_t under = (uint32_t)(t >> 31);                           // t < 0
   const uint32_t over = (uint32_t)(((1 << (wE + wF)) - 1 - t) >> 31);   // t >= 2^(wE+wF)
   const uint32_t nan = (uint32_t)((int)(0x7F800000u - a) >> 31);        // a > 0x7F800000
   uint32_t code = (1u << sh_x) | sgn | (uint32_t)t;
-  code = (code & ~under) | (sgn & under);                       // underflow, +-0
-  code = (code & ~over) | (((2u << sh_x) | sgn) & over);        // overflow, +-inf
-  code = (code & ~nan) | ((3u << sh_x) & nan);                  // NaN
-  return code;
+  code = __builtin_amdgcn_bitop3_b32(under, sgn, code, 0xCA);                   // +-0
+  code = __builtin_amdgcn_bitop3_b32(over, (2u << sh_x) | sgn, code, 0xCA);     // +-inf
+  return __builtin_amdgcn_bitop3_b32(nan, 3u << sh_x, code, 0xCA);              // NaN
+}
+
+// code of (wE, wF) -> float32 bits for wE <= 7, where every value of the
+// format is a normal float32 (the result is exact): exponent E + 127 - bias,
+// fraction F << (23 - wF), +-0, +-inf, and NaN as 0x7FC00000, all selected
+// with masks of the exception bits, without branches.
+__device__ __forceinline__ uint32_t decode_narrow(uint32_t code, int wE, int wF) {
+  const int sh_s = wF + wE;
+  const uint32_t e = __builtin_amdgcn_ubfe(code, wF, wE) + (uint32_t)(127 - ((1 << (wE - 1)) - 1));
+  const uint32_t v = (e << 23) | ((code << (23 - wF)) & 0x7FFFFFu);   // the normal value
+  const uint32_t sbit = (code >> sh_s) << 31;
+  const uint32_t x0 = (uint32_t)__builtin_amdgcn_sbfe((int)code, sh_s + 1, 1);  // all ones if set
+  const uint32_t x1 = (uint32_t)__builtin_amdgcn_sbfe((int)code, sh_s + 2, 1);
+  const uint32_t lo = x0 & v;                                    // x1 = 0: normal or zero
+  const uint32_t hi = 0x7F800000u | (x0 & 0x00400000u);          // x1 = 1: inf or NaN
+  const uint32_t mag = __builtin_amdgcn_bitop3_b32(x1, hi, lo, 0xCA);
+  // the sign, except on NaN: s & ~(x0 & x1) (bitop3 of (s, x0, x1))
+  return mag | __builtin_amdgcn_bitop3_b32(sbit, x0, x1, 0x70);
 }
 
 // code of (wE, wF) -> float32 bits (exact unless wE = 8 reaches float32's

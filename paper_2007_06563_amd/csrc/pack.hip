@@ -13,11 +13,16 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "codec.hpp"
 #include "pack.hpp"
 
 namespace hobflops {
+
+typedef __attribute__((address_space(3))) uint32_t lds_word;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));  // one 16-byte access
+typedef __attribute__((address_space(3))) u32x4 lds_u32x4;
 
 // Groups of 32 values a wave handles: two per pass (lanes 0-31, 32-63), U
 // passes whose loads are all issued before any value is quantised, so a wave
@@ -35,11 +40,14 @@ constexpr int kUMax = kULarge;
 // group come from a division by G, in 32-bit arithmetic when the group count
 // allows (kIdxNarrow).
 constexpr int kIdxNarrow = 0, kIdxWide = 1, kIdxDense = 2;
+// Dense, with 16-byte aligned value and plane arrays: a wave moves its values
+// and its plane words with 16-byte accesses through LDS (kIdxDenseVec).
+constexpr int kIdxDenseVec = 3;
 
 template <int kIdx>
 __device__ __forceinline__ int64_t value_index(int64_t q, int j, int G, int64_t len,
                                                bool& in_row) {
-  if (kIdx == kIdxDense) {
+  if (kIdx == kIdxDense || kIdx == kIdxDenseVec) {
     in_row = true;
     return q * 32 + j;
   }
@@ -64,6 +72,7 @@ __device__ __forceinline__ int64_t value_index(int64_t q, int j, int G, int64_t 
 // its partner's bits i + d into positions i. A stage is one cross-lane read
 // (ds_swizzle, xor mode, no memory access), one rotate and one bit select; the
 // per-lane rotate amounts and masks are set up once (lane_transpose_setup).
+// The bit select is one v_bitop3_b32 (truth table 0xCA: mask ? r : x).
 struct LaneT {
   uint32_t rot[5], mask[5];
 };
@@ -96,7 +105,7 @@ __device__ __forceinline__ void lane_transpose(uint32_t (&x)[U], const LaneT& t)
     _Pragma("unroll") for (int u = 0; u < U; ++u) p[u] = xor_lane<S>(x[u]);     \
     _Pragma("unroll") for (int u = 0; u < U; ++u) {                             \
       const uint32_t r = __builtin_amdgcn_alignbit(p[u], p[u], t.rot[S]);       \
-      x[u] = (r & t.mask[S]) | (x[u] & ~t.mask[S]);                             \
+      x[u] = __builtin_amdgcn_bitop3_b32(t.mask[S], r, x[u], 0xCA);             \
     }                                                                           \
   }
   HOBFLOPS_STAGE(0)
@@ -139,6 +148,103 @@ __device__ __forceinline__ void value_indices(const PackRange& R, int64_t wave, 
   }
 }
 
+// Decoder of one pass set to float32 bits, or codes kept (uniform branch on
+// the destination kind and format).
+template <int U>
+__device__ __forceinline__ void decode_all(uint32_t (&x)[U], int kind, int wE, int wF) {
+  if (kind != 0) return;
+  if (wE <= 7) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = decode_narrow(x[u], wE, wF);
+  } else {
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = decode_bits(x[u], wE, wF);
+  }
+}
+
+// Quantiser of one pass set (uniform branch on the source kind and format).
+template <int NB, int U>
+__device__ __forceinline__ void quantize_all(uint32_t (&x)[U], const bool (&have)[U], int kind,
+                                             int wE, int wF) {
+  constexpr uint32_t nbmask = NB >= 32 ? 0xFFFFFFFFu : ((1u << (NB & 31)) - 1u);
+  if (kind != 0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = have[u] ? (x[u] & nbmask) : 0u;
+  } else if (wE <= 7 && wF <= 22) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = have[u] ? quantize_narrow(x[u], wE, wF) : 0u;
+  } else {
+#pragma unroll
+    for (int u = 0; u < U; ++u) x[u] = have[u] ? quantize_bits(x[u], wE, wF) : 0u;
+  }
+}
+
+// Dense ranges with 16-byte aligned arrays (kIdxDenseVec), whole chunks of
+// 2U groups (64U values) only: a wave takes kChunksPerWave consecutive chunks
+// and keeps the next two chunks' loads in flight while it works on one, so
+// that memory stays busy through the quantiser and the transpose. A chunk's
+// values come in with 16-byte loads, go through this wave's LDS buffer so
+// that each lane takes value j of its half's group per pass, and after the
+// transpose the plane words go back through the same buffer and out with
+// 16-byte stores. Nothing in the chunk path branches on data, so the waits
+// for a load count only the loads before it. A range's last groups that do
+// not fill a chunk form a range of their own (the per-value path). LDS
+// operations of one wave complete in order, so only the compiler needs to be
+// kept from reordering them (wave barriers).
+constexpr int kChunksPerWave = 2;
+
+template <int U>
+struct ChunkRegs {
+  u32x4 v[U / 4];  // one chunk's 16U 16-byte units, U/4 per lane
+};
+
+// Requests chunk `chunk` of the range, clamped to the range's last chunk (a
+// request past the end loads data that is not used).
+template <int U>
+__device__ __forceinline__ void pack_load_chunk(const PackRange& R, int64_t chunk, int lane,
+                                                ChunkRegs<U>& r) {
+  const int64_t last = (R.q1 - R.q0) / (2 * U) - 1;
+  const u32x4* src =
+      reinterpret_cast<const u32x4*>(R.src) + (R.q0 + min(chunk, last) * 2 * U) * 8;
+#pragma unroll
+  for (int k = 0; k < U / 4; ++k) r.v[k] = src[lane + 64 * k];
+}
+
+template <int NB, int U>
+__device__ __forceinline__ void pack_process_chunk(const PackRange& R, int64_t chunk, int lane,
+                                                   int wE, int wF, const ChunkRegs<U>& r,
+                                                   lds_word* buf) {
+  const int64_t qw0 = R.q0 + chunk * 2 * U;
+  if (qw0 >= R.q1) return;  // past the range (uniform)
+  constexpr int kWords = 2 * U * NB;  // plane words of a chunk
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int k = 0; k < U / 4; ++k) reinterpret_cast<lds_u32x4*>(buf)[lane + 64 * k] = r.v[k];
+  __builtin_amdgcn_wave_barrier();
+  const int j = lane & 31, h = lane >> 5;
+  uint32_t x[U];
+  bool have[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    x[u] = buf[64 * u + lane];
+    have[u] = true;
+  }
+  __builtin_amdgcn_wave_barrier();  // every value read before the buffer is rewritten
+  quantize_all<NB, U>(x, have, R.kind, wE, wF);
+  lane_transpose(x, lane_transpose_setup(j));
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (j < NB) buf[(2 * u + h) * NB + j] = x[u];
+  __builtin_amdgcn_wave_barrier();
+  u32x4* dst = reinterpret_cast<u32x4*>(R.planes + qw0 * NB);
+#pragma unroll
+  for (int k = 0; k < (kWords / 4 + 63) / 64; ++k) {
+    const int unit = lane + 64 * k;
+    if (kWords / 4 % 64 == 0 || unit < kWords / 4)
+      dst[unit] = reinterpret_cast<const lds_u32x4*>(buf)[unit];
+  }
+}
+
 template <int NB, int U>
 __global__ __launch_bounds__(256) void pack_kernel(const PackLaunch L, int wE, int wF) {
   const int lane = threadIdx.x & 63;
@@ -146,11 +252,28 @@ __global__ __launch_bounds__(256) void pack_kernel(const PackLaunch L, int wE, i
   // range's fields and the mode branches stay scalar
   const int64_t wave = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int j = lane & 31;
-  constexpr uint32_t nbmask = NB >= 32 ? 0xFFFFFFFFu : ((1u << (NB & 31)) - 1u);
   int k = 0;
 #pragma unroll
   for (int t = 1; t < kMaxJobs; ++t) k = (t < L.count && wave >= L.r[t].wave0) ? t : k;
   const PackRange& R = L.r[k];
+  if (R.idx == kIdxDenseVec) {  // uniform branch
+    __shared__ uint32_t stage[4][64 * U > 2 * U * NB ? 64 * U : 2 * U * NB];
+    lds_word* buf = (lds_word*)stage[threadIdx.x >> 6];
+    const int64_t c0 = (wave - R.wave0) * kChunksPerWave;
+    // two register sets, alternating (the loop is unrolled by two so that no
+    // set still being loaded is copied)
+    ChunkRegs<U> ra, rb;
+    pack_load_chunk<U>(R, c0, lane, ra);
+    pack_load_chunk<U>(R, c0 + 1, lane, rb);
+#pragma unroll
+    for (int c = 0; c < kChunksPerWave; c += 2) {
+      pack_process_chunk<NB, U>(R, c0 + c, lane, wE, wF, ra, buf);
+      if (c + 2 < kChunksPerWave) pack_load_chunk<U>(R, c0 + c + 2, lane, ra);
+      pack_process_chunk<NB, U>(R, c0 + c + 1, lane, wE, wF, rb, buf);
+      if (c + 3 < kChunksPerWave) pack_load_chunk<U>(R, c0 + c + 3, lane, rb);
+    }
+    return;
+  }
   int64_t idx[U];
   bool have[U];
   if (R.idx == kIdxDense)  // uniform branch
@@ -165,16 +288,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const PackLaunch L, int wE, i
 #pragma unroll
   for (int u = 0; u < U; ++u) x[u] = ((const uint32_t*)R.src)[idx[u]];
   // one uniform branch for the whole pass set
-  if (R.kind != 0) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) x[u] = have[u] ? (x[u] & nbmask) : 0u;
-  } else if (wE <= 7) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) x[u] = have[u] ? quantize_narrow(x[u], wE, wF) : 0u;
-  } else {
-#pragma unroll
-    for (int u = 0; u < U; ++u) x[u] = have[u] ? quantize_bits(x[u], wE, wF) : 0u;
-  }
+  quantize_all<NB, U>(x, have, R.kind, wE, wF);
   // lane j of each half now holds plane j of its group
   lane_transpose(x, lane_transpose_setup(j));
 #pragma unroll
@@ -182,6 +296,66 @@ __global__ __launch_bounds__(256) void pack_kernel(const PackLaunch L, int wE, i
     const int64_t q = R.q0 + ((wave - R.wave0) * U + u) * 2 + (lane >> 5);
     if (q < R.q1 && j < NB) R.planes[q * NB + j] = x[u];
   }
+}
+
+// The unpack of dense tensors with 16-byte aligned arrays, whole chunks of 2U
+// groups only (the mirror of the pack's; the groups after the last whole
+// chunk go to the per-value path): a wave takes kChunksPerWave consecutive
+// chunks, with the next two chunks' plane words in flight while it works on
+// one. A chunk's words come in with 16-byte loads, go through LDS so that
+// each lane takes plane j of its half's group per pass, and after the
+// transpose and the decode the 64U values go back through LDS and out with
+// 16-byte stores.
+template <int NB, int U>
+struct PlaneRegs {
+  u32x4 v[(2 * U * NB / 4 + 63) / 64];  // one chunk's plane words, 16 bytes a unit
+};
+
+template <int NB, int U>
+__device__ __forceinline__ void unpack_load_chunk(const uint32_t* __restrict__ planes,
+                                                  int64_t nchunks, int64_t chunk, int lane,
+                                                  PlaneRegs<NB, U>& r) {
+  constexpr int kUnits = 2 * U * NB / 4;
+  // clamped: a request past the end loads a chunk that is not used
+  const u32x4* src =
+      reinterpret_cast<const u32x4*>(planes + min(chunk, nchunks - 1) * 2 * U * NB);
+#pragma unroll
+  for (int k = 0; k < (kUnits + 63) / 64; ++k) {
+    const int unit = lane + 64 * k;
+    r.v[k] = src[kUnits % 64 == 0 ? unit : min(unit, kUnits - 1)];
+  }
+}
+
+template <int NB, int U>
+__device__ __forceinline__ void unpack_process_chunk(int64_t nchunks, int64_t chunk, int lane,
+                                                     int kind, int wE, int wF,
+                                                     const PlaneRegs<NB, U>& r,
+                                                     uint32_t* __restrict__ dst, lds_word* buf) {
+  constexpr int kUnits = 2 * U * NB / 4;
+  if (chunk >= nchunks) return;  // past the end (uniform)
+  __builtin_amdgcn_wave_barrier();
+#pragma unroll
+  for (int k = 0; k < (kUnits + 63) / 64; ++k) {
+    const int unit = lane + 64 * k;
+    if (kUnits % 64 == 0 || unit < kUnits) reinterpret_cast<lds_u32x4*>(buf)[unit] = r.v[k];
+  }
+  __builtin_amdgcn_wave_barrier();
+  const int j = lane & 31, h = lane >> 5;
+  uint32_t x[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const uint32_t v = buf[(2 * u + h) * NB + min(j, NB - 1)];
+    x[u] = j < NB ? v : 0u;
+  }
+  __builtin_amdgcn_wave_barrier();  // every word read before the buffer is rewritten
+  lane_transpose(x, lane_transpose_setup(j));
+  decode_all<U>(x, kind, wE, wF);
+#pragma unroll
+  for (int u = 0; u < U; ++u) buf[64 * u + lane] = x[u];
+  __builtin_amdgcn_wave_barrier();
+  u32x4* d = reinterpret_cast<u32x4*>(dst) + chunk * 16 * U;
+#pragma unroll
+  for (int k = 0; k < U / 4; ++k) d[lane + 64 * k] = reinterpret_cast<const lds_u32x4*>(buf)[lane + 64 * k];
 }
 
 template <int NB, int kIdx, int U>
@@ -192,6 +366,25 @@ __global__ __launch_bounds__(256) void unpack_kernel(const uint32_t* __restrict_
   const int lane = threadIdx.x & 63;
   const int64_t wave = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const int j = lane & 31;
+  if constexpr (kIdx == kIdxDenseVec) {  // ngroups is a whole number of chunks here
+    __shared__ uint32_t stage[4][64 * U > 2 * U * NB ? 64 * U : 2 * U * NB];
+    lds_word* buf = (lds_word*)stage[threadIdx.x >> 6];
+    const int64_t nchunks = ngroups / (2 * U);
+    const int64_t c0 = __builtin_amdgcn_readfirstlane((int)(wave & 0x7FFFFFFF)) *
+                       (int64_t)kChunksPerWave;
+    PlaneRegs<NB, U> ra, rb;
+    unpack_load_chunk<NB, U>(planes, nchunks, c0, lane, ra);
+    unpack_load_chunk<NB, U>(planes, nchunks, c0 + 1, lane, rb);
+#pragma unroll
+    for (int c = 0; c < kChunksPerWave; c += 2) {
+      unpack_process_chunk<NB, U>(nchunks, c0 + c, lane, kind, wE, wF, ra, (uint32_t*)dst, buf);
+      if (c + 2 < kChunksPerWave) unpack_load_chunk<NB, U>(planes, nchunks, c0 + c + 2, lane, ra);
+      unpack_process_chunk<NB, U>(nchunks, c0 + c + 1, lane, kind, wE, wF, rb, (uint32_t*)dst,
+                                  buf);
+      if (c + 3 < kChunksPerWave) unpack_load_chunk<NB, U>(planes, nchunks, c0 + c + 3, lane, rb);
+    }
+    return;
+  }
   uint32_t x[U];
 #pragma unroll
   for (int u = 0; u < U; ++u) {  // lane j < NB: plane j of its group (clamped load)
@@ -201,6 +394,7 @@ __global__ __launch_bounds__(256) void unpack_kernel(const uint32_t* __restrict_
   }
   // the transpose is its own inverse: lane j now holds the code at column 32g + j
   lane_transpose(x, lane_transpose_setup(j));
+  decode_all<U>(x, kind, wE, wF);
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int64_t q = (wave * U + u) * 2 + (lane >> 5);
@@ -208,19 +402,20 @@ __global__ __launch_bounds__(256) void unpack_kernel(const uint32_t* __restrict_
     bool in_row;
     const int64_t i = value_index<kIdx>(q, j, G, len, in_row);
     if (!in_row) continue;
-    ((uint32_t*)dst)[i] = kind == 0 ? decode_bits(x[u], wE, wF) : x[u];
+    ((uint32_t*)dst)[i] = x[u];
   }
 }
 
 namespace {
 
-// NB = 3 + wE + wF runs from 6 to 32; f gets the kernel types of the three
+// NB = 3 + wE + wF runs from 6 to 32; f gets the kernel types of the four
 // index modes.
 template <template <int, int> class K, int NB = 6>
 struct nb_dispatch {
   template <class F>
   static hipError_t run(int nb, F&& f) {
-    if (nb == NB) return f(K<NB, kIdxNarrow>{}, K<NB, kIdxWide>{}, K<NB, kIdxDense>{});
+    if (nb == NB)
+      return f(K<NB, kIdxNarrow>{}, K<NB, kIdxWide>{}, K<NB, kIdxDense>{}, K<NB, kIdxDenseVec>{});
     return nb_dispatch<K, NB + 1>::run(nb, f);
   }
 };
@@ -258,23 +453,31 @@ struct UnpackU {
 
 }  // namespace
 
-// Index mode of a tensor: dense when the row length is a multiple of 32, else
-// 32-bit division when the group count allows.
-static int index_mode(int64_t len, int64_t ngroups) {
-  if (len % 32 == 0) return kIdxDense;
+// Index mode of a tensor: dense when the row length is a multiple of 32 (with
+// 16-byte accesses when both arrays allow them: vec), else 32-bit division
+// when the group count allows.
+static int index_mode(int64_t len, int64_t ngroups, bool vec = false) {
+  if (len % 32 == 0) return vec ? kIdxDenseVec : kIdxDense;
   return ngroups + 2 * kUMax >= ((int64_t)1 << 31) ? kIdxWide : kIdxNarrow;
 }
 
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
 // The unpack kernel of the tensor's index mode, U passes a wave.
 template <int U, template <int, int> class K, class... Args>
-static hipError_t launch_groups(int NB, int64_t len, int64_t ngroups, hipStream_t stream,
-                                Args... args) {
-  const int64_t waves = (ngroups + 2 * U - 1) / (2 * U);
+static hipError_t launch_groups(int NB, int64_t len, int64_t ngroups, bool vec,
+                                hipStream_t stream, Args... args) {
+  const int mode = index_mode(len, ngroups, vec);
+  const int64_t chunks = (ngroups + 2 * U - 1) / (2 * U);
+  const int64_t waves =
+      mode == kIdxDenseVec ? (chunks + kChunksPerWave - 1) / kChunksPerWave : chunks;
   const int64_t blocks = (waves + 3) / 4;
   if (blocks == 0) return hipSuccess;
-  const int mode = index_mode(len, ngroups);
-  return nb_dispatch<K>::run(NB, [&](auto narrow_k, auto wide_k, auto dense_k) {
-    if (mode == kIdxDense)
+  return nb_dispatch<K>::run(NB, [&](auto narrow_k, auto wide_k, auto dense_k, auto vec_k) {
+    if (mode == kIdxDenseVec)
+      hipLaunchKernelGGL(decltype(vec_k)::fn, dim3((unsigned)blocks), dim3(256), 0, stream,
+                         args...);
+    else if (mode == kIdxDense)
       hipLaunchKernelGGL(decltype(dense_k)::fn, dim3((unsigned)blocks), dim3(256), 0, stream,
                          args...);
     else if (mode == kIdxWide)
@@ -317,9 +520,27 @@ hipError_t launch_pack_batch(const PackTensor* t, int count, int wE, int wF, hip
         const hipError_t e = flush();
         if (e != hipSuccess) return e;
       }
-      L.r[L.count++] = PackRange{t[n].src, t[n].planes, t[n].len, q0, q1, waves, (int)G,
-                                 t[n].kind, index_mode(t[n].len, ngroups)};
-      waves += nw;
+      // 16-byte accesses where the range's values and planes both start
+      // 16-byte aligned (a range start is a multiple of 2^25 groups), for its
+      // whole chunks of 2U groups; the groups after them, if any, form a range
+      // of their own
+      const bool vec = aligned16(t[n].src) && aligned16(t[n].planes + q0 * NB);
+      const int mode = index_mode(t[n].len, ngroups, vec);
+      const int64_t qv = mode == kIdxDenseVec ? q0 + (q1 - q0) / (2 * U) * 2 * U : q0;
+      if (qv > q0) {
+        L.r[L.count++] = PackRange{t[n].src, t[n].planes, t[n].len, q0, qv, waves, (int)G,
+                                   t[n].kind, kIdxDenseVec};
+        waves += ((qv - q0) / (2 * U) + kChunksPerWave - 1) / kChunksPerWave;
+      }
+      if (q1 > qv) {
+        if (L.count == kMaxJobs) {
+          const hipError_t e = flush();
+          if (e != hipSuccess) return e;
+        }
+        L.r[L.count++] = PackRange{t[n].src, t[n].planes, t[n].len, qv, q1, waves, (int)G,
+                                   t[n].kind, index_mode(t[n].len, ngroups, false)};
+        waves += (q1 - qv + 2 * U - 1) / (2 * U);
+      }
     }
   }
   return flush();
@@ -335,11 +556,26 @@ hipError_t launch_unpack(const uint32_t* planes, int64_t rows, int64_t len, int 
                          int kind, void* dst, hipStream_t stream) {
   const int64_t G = (len + 31) / 32;
   const int64_t ngroups = rows * G;
-  if (ngroups >= kLargeGroups)
-    return launch_groups<kULarge, UnpackU<kULarge>::K>(3 + wE + wF, len, ngroups, stream, planes,
-                                                      kind, len, (int)G, wE, wF, dst, ngroups);
-  return launch_groups<kUSmall, UnpackU<kUSmall>::K>(3 + wE + wF, len, ngroups, stream, planes,
-                                                    kind, len, (int)G, wE, wF, dst, ngroups);
+  const int NB = 3 + wE + wF;
+  // dense with 16-byte aligned arrays: whole chunks of 2U groups with 16-byte
+  // accesses, the groups after them (if any) per value, in a second launch
+  const bool vec = len % 32 == 0 && aligned16(planes) && aligned16(dst);
+  auto run = [&](auto u_tag) -> hipError_t {
+    constexpr int U = decltype(u_tag)::value;
+    const int64_t qv = vec ? ngroups / (2 * U) * 2 * U : 0;
+    if (qv > 0) {
+      const hipError_t e = launch_groups<U, UnpackU<U>::template K>(NB, len, qv, true, stream, planes,
+                                                          kind, len, (int)G, wE, wF, dst, qv);
+      if (e != hipSuccess) return e;
+    }
+    if (qv == ngroups) return hipSuccess;
+    // the rest: dense groups from qv on (values 32 qv on), or the whole tensor
+    return launch_groups<U, UnpackU<U>::template K>(NB, len, ngroups - qv, false, stream,
+                                          planes + qv * NB, kind, len, (int)G, wE, wF,
+                                          (void*)((uint32_t*)dst + qv * 32), ngroups - qv);
+  };
+  if (ngroups >= kLargeGroups) return run(std::integral_constant<int, kULarge>{});
+  return run(std::integral_constant<int, kUSmall>{});
 }
 
 }  // namespace hobflops

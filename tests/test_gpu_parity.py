@@ -141,6 +141,48 @@ def test_pack_every_float32_pattern():
             del i, bits, planes, codes, h
 
 
+@pytest.mark.parametrize("wE,wF", [(5, 3), (8, 7), (5, 10), (6, 23)])
+def test_pack_unpack_16_byte_paths_and_fallbacks(wE, wF):
+    """Dense tensors move 16 bytes per lane through LDS when both arrays are
+    16-byte aligned; a large launch (eight passes a wave) whose last wave is
+    partial, and sources or destinations only 4-byte aligned (the per-value
+    path), all against the oracle."""
+    hf = need_gpu()
+    nb = 3 + wE + wF
+    groups = (1 << 18) + 5           # eight passes a wave, last wave partial
+    n = 32 * groups
+    x = rand_f32(900 + wF, n + 4)
+    xd = dev(x)
+    sel = np.r_[0:64, groups - 40:groups]               # first waves and the partial tail
+    vsel = (32 * sel[:, None] + np.arange(32)).reshape(-1)
+    for off in (0, 1):               # off 1: source 4-byte aligned only
+        say(f"pack 16-byte path fmt=({wE},{wF}) groups={groups} src offset={off}")
+        want = orc.quantize_f32(x[off + vsel], wE, wF)
+        src = xd[off:off + n].view(1, n)
+        planes = hf.pack(src, (wE, wF))
+        torch.cuda.synchronize()
+        got = planes.cpu().numpy().view(np.uint32).reshape(-1, nb)
+        assert np.array_equal(got[sel], pack_codes(want.reshape(1, -1), nb).reshape(-1, nb))
+        for doff in (0, 1):          # doff 1: destination 4-byte aligned only
+            say(f"unpack 16-byte path fmt=({wE},{wF}) dst offset={doff}")
+            buf = torch.empty(n + 4, dtype=torch.int32, device="cuda")
+            out = buf[doff:doff + n].view(1, n)
+            hf.unpack(planes, 1, n, (wE, wF), kind="code", out=out)
+            torch.cuda.synchronize()
+            codes = codes_of(out)[0]
+            assert np.array_equal(codes[vsel], want)
+    # a multiple of 16 groups with every value checked, small launch (four passes)
+    m = 32 * 16 * 9
+    want = orc.quantize_f32(x[:m], wE, wF)
+    xs = dev(x[:m].reshape(9, -1))
+    planes = hf.pack(xs, (wE, wF))
+    vals = hf.unpack(planes, 9, m // 9, (wE, wF), kind="f32")
+    torch.cuda.synchronize()
+    assert np.array_equal(planes.cpu().numpy().view(np.uint32), pack_codes(want.reshape(9, -1), nb))
+    assert np.array_equal(vals.cpu().numpy().view(np.uint32).reshape(-1),
+                          orc.decode_f32(want, wE, wF).view(np.uint32))
+
+
 @pytest.mark.parametrize("njobs", [5, 11])
 @pytest.mark.parametrize("wE,wF", [(5, 3), (8, 7), (4, 2)])
 def test_pack_batch_equals_single_packs(wE, wF, njobs):
