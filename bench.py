@@ -55,7 +55,7 @@ IN_FMT, ACC_FMT, OUT_FMT = (5, 3), (5, 4), (5, 4)
 # counter reads for a plain 256 MiB device copy (FETCH x2.0, WRITE x1.0); see
 # the profiles/ summaries. Set to None whenever the kernel changes, until the
 # counters are taken again.
-TRAFFIC = (3566.0 * 2.0 + 6272.7 * 1.0) * 1024   # 13.73 MB (split kernel, float32 OFM)
+TRAFFIC = (3559.9 * 2.0 + 6272.4 * 1.0) * 1024   # 13.71 MB (split kernel, float32 OFM)
 
 
 def log(*a):
@@ -183,6 +183,47 @@ def pack_bench(reps):
                         f"{nbytes} algorithmic bytes", "kernel": name, "ms": ms,
             "roofline": {"bound": "hbm", "achieved": nbytes / (ms * 1e-3) / 1e9, "peak": 8000.0,
                          "unit": "GB/s", "frac": nbytes / (ms * 1e-3) / HBM_PEAK}}), flush=True)
+
+
+PROBE_KINDS = ["v_bitop3_b32 (8 bytes), sources in three VGPR banks, independent",
+               "v_bitop3_b32, two sources in one VGPR bank, independent",
+               "v_xor_b32 (VOP2, 4 bytes), sources in two banks, independent",
+               "v_bitop3_b32, three banks, 1024 instructions per loop branch",
+               "v_bitop3_b32, three banks, each reading the previous result",
+               "v_bitop3_b32 and v_xor_b32 alternating, independent",
+               "v_bitop3_b32, three banks, each reading the result two back",
+               "v_bitop3_b32, three banks, each reading the result four back",
+               "v_bitop3_b32, three banks, every instruction 8-byte aligned",
+               "groups of one v_xor_b32 and seven v_bitop3_b32, every other group misaligned",
+               "groups of v_xor_b32, seven v_bitop3_b32 and s_nop 0, all aligned"]
+
+
+def issue_rate(iters):
+    """The VALU issue-rate probe (csrc/issue_probe.hip): one JSON line per
+    instruction stream and waves per CU (one workgroup per CU): how often one
+    wave issues, how often one SIMD does, and the shader clock meanwhile. The
+    single-wave interval is what the convolution's issue_ceiling rests on."""
+    import ctypes
+    from paper_2007_06563_amd import build as B
+    L = ctypes.CDLL(B.PROBE_LIB)
+    dbl = ctypes.POINTER(ctypes.c_double)
+    L.hobflops_probe_issue.argtypes = [ctypes.c_int] * 4 + [dbl] * 3
+    L.hobflops_probe_issue.restype = ctypes.c_int
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    runs = [(k, 1) for k in range(len(PROBE_KINDS))]
+    runs += [(k, w) for k in (8, 1, 2, 4) for w in (2, 4, 8, 16)]
+    for kind, waves in runs:
+        a, b, c = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+        rc = L.hobflops_probe_issue(cus, waves, kind, iters, ctypes.byref(a),
+                                    ctypes.byref(b), ctypes.byref(c))
+        if rc != 0:
+            raise RuntimeError(f"issue probe failed: {rc}")
+        print(json.dumps({
+            "probe": "VALU issue rate", "stream": PROBE_KINDS[kind], "kind": kind,
+            "waves_per_cu": waves, "waves_per_simd": -(-waves // 4),
+            "clocks_per_instr_per_wave": round(a.value, 4),
+            "clocks_per_instr_per_simd": round(b.value, 4),
+            "shader_ghz": round(c.value, 4)}), flush=True)
 
 
 def suite(reps, only=None):
@@ -397,6 +438,9 @@ def main():
                          "(element-wise sweep, mantissa sweep, 13-layer stack)")
     ap.add_argument("--only", default=None,
                     help="with --suite: only the workloads whose label contains this text")
+    ap.add_argument("--issue-rate", action="store_true",
+                    help="instead of the one-line benchmark: the VALU issue-rate probe, one JSON "
+                         "line per waves-per-CU and bank pattern")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the layer shards "
@@ -407,6 +451,9 @@ def main():
     dev = torch.device("cuda:0")
     if args.suite:
         suite(args.steps, args.only)
+        return
+    if args.issue_rate:
+        issue_rate(400)
         return
     if args.pack:
         pack_bench(args.steps)

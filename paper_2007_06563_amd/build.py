@@ -10,6 +10,7 @@ import concurrent.futures as cf
 import hashlib
 import json
 import os
+import shlex
 import shutil
 import subprocess
 import sys
@@ -19,6 +20,8 @@ ROOT = os.path.dirname(HERE)
 GEN = os.path.join(HERE, "_gen")
 OBJ = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhobflops.so")
+# the VALU issue-rate probe (a diagnostic for the roofline, bench.py --issue-rate)
+PROBE_LIB = os.path.join(HERE, "libhobflops_probe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 HIPFLAGS = ["-O3", "--offload-arch=gfx950", "-std=c++17", "-fPIC",
             "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
@@ -28,7 +31,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 from paper_2007_06563_amd import variants  # noqa: E402
-from paper_2007_06563_amd.gen import asmgen, emit, fp, opt, regalloc  # noqa: E402
+from paper_2007_06563_amd.gen import align, asmgen, emit, fp, opt, regalloc  # noqa: E402
 
 
 def nb(wE, wF):
@@ -468,11 +471,69 @@ hipError_t launch_pool_{tag}(const uint32_t* in, uint32_t* out, const PoolParams
     return [os.path.join(GEN, n) for n, _ in files]
 
 
-def _compile(src, obj):
+LLVM_MC = "/opt/rocm/llvm/bin/llvm-mc"
+# Kernels the alignment pass is applied to (mangled names, as in the code
+# section names): measured faster with it (element-wise muladd up to 11 %,
+# pooling 5 %) or no slower. The fused conv and the unpack kernel run many
+# waves per SIMD, which hide a wave's misaligned fetches, and measured up to
+# 5 % slower with the pass's re-encodings and nops; they are left as compiled.
+ALIGN_KERNELS = ("19conv2d_split_kernel", "13muladd_kernel", "14avgpool_kernel", "11pack_kernel")
+
+
+def _compile_plain(src, obj):
     cmd = [HIPCC] + HIPFLAGS + ["-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr[-4000:]}")
+    return obj
+
+
+def _compile(src, obj, stats=None):
+    """hipcc -c, with the device code taken through assembly text so that
+    gen/align.py can keep its 8-byte instructions 8-byte aligned: the
+    driver's own steps (hipcc -###) are run one by one, the device step
+    writing assembly instead of an object, which is aligned and assembled
+    into the object the later steps (link, bundle, host compile) expect."""
+    r = subprocess.run([HIPCC, "-###"] + HIPFLAGS + ["-c", src, "-o", obj],
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc -### failed on {src}:\n{r.stderr[-4000:]}")
+    cmds = [shlex.split(line) for line in r.stderr.splitlines() if line.startswith(' "')]
+    dev = [c for c in cmds if "-fcuda-is-device" in c and "-emit-obj" in c]
+    if len(dev) != 1:
+        raise RuntimeError(f"unexpected hipcc pipeline for {src}: {len(dev)} device steps")
+    dev = dev[0]
+    k = dev.index("-o")
+    dev_obj = dev[k + 1]
+    asm, fixed = obj + ".dev.s", obj + ".dev.aligned.s"
+    to_asm = list(dev)
+    to_asm[to_asm.index("-emit-obj")] = "-S"
+    to_asm[k + 1] = asm
+    temps = [asm, fixed] + [c[c.index("-o") + 1] for c in cmds if "-o" in c and c is not cmds[-1]]
+    temps += [a.split("=", 1)[1] for c in cmds for a in c if a.startswith("-output=")]
+    try:
+        for c in cmds:
+            if c is dev:
+                r = subprocess.run(to_asm, capture_output=True, text=True)
+                if r.returncode != 0:
+                    raise RuntimeError(f"device compile failed on {src}:\n{r.stderr[-4000:]}")
+                text = open(asm).read()
+                new, st = align.align_text(text, align.encoding_sizes(asm, LLVM_MC),
+                                           only=ALIGN_KERNELS)
+                with open(fixed, "w") as f:
+                    f.write(new)
+                c = [LLVM_MC, "-triple=amdgcn-amd-amdhsa", "-mcpu=gfx950", "-filetype=obj",
+                     "-o", dev_obj, fixed]
+                if stats is not None:
+                    stats[os.path.basename(src)] = st
+            r = subprocess.run(c, capture_output=True, text=True)
+            if r.returncode != 0:
+                raise RuntimeError(f"{os.path.basename(c[0])} failed on {src}:\n"
+                                   f"{r.stderr[-4000:]}")
+    finally:
+        for t in temps:
+            if t != obj and os.path.exists(t):
+                os.remove(t)
     return obj
 
 
@@ -482,22 +543,35 @@ def build(jobs=None, verbose=True):
     srcs = [os.path.join(HERE, "csrc", "abi.hip"), os.path.join(HERE, "csrc", "pack.hip")] + gen_files
     os.makedirs(OBJ, exist_ok=True)
     jobs = jobs or min(16, os.cpu_count() or 4)
-    objs = []
+    objs, stats = [], {}
     with cf.ThreadPoolExecutor(jobs) as ex:
         futs = []
         for s in srcs:
             o = os.path.join(OBJ, os.path.basename(s) + ".o")
-            futs.append(ex.submit(_compile, s, o))
+            futs.append(ex.submit(_compile, s, o, stats))
         for f in futs:
             objs.append(f.result())
+    if verbose:
+        tot = {k: sum(st[k] for st in stats.values()) for k in ("promoted", "nops", "left")}
+        print(f"8-byte alignment: {tot['promoted']} VALU instructions re-encoded as VOP3, "
+              f"{tot['nops']} s_nop inserted, {tot['left']} short runs left")
     tmp = LIB + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr[-4000:]}")
     os.replace(tmp, LIB)
+    # the probe's misaligned streams are deliberate: no alignment pass
+    probe_obj = _compile_plain(os.path.join(HERE, "csrc", "issue_probe.hip"),
+                               os.path.join(OBJ, "issue_probe.hip.o"))
+    tmp = PROBE_LIB + ".tmp"
+    r = subprocess.run([HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp, probe_obj],
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stderr[-4000:]}")
+    os.replace(tmp, PROBE_LIB)
     if verbose:
-        print("built", LIB)
+        print("built", LIB, "and", PROBE_LIB)
     return LIB
 
 
