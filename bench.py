@@ -41,10 +41,10 @@ N_SIMD = N_CU * 4
 HBM_PEAK = 8.0e12
 # clocks per instruction of one wave with a SIMD to itself (measured on MI355X
 # with the split kernel's accumulator loop alone in the kernel, shader-clock
-# stamps around the loop: 4.44; a synthetic stream of 8-byte v_bitop3_b32
-# measures 4.54 per instruction including its loop branch), and of a SIMD
-# shared by two or more waves of bank-conflict-free bitwise instructions
-# (2.24-2.36: the peak assumes 2)
+# stamps around the loop: 4.44; the issue-rate probe's aligned 8-byte
+# v_bitop3_b32 stream: 4.26 including its loop branch), and of a SIMD shared
+# by two or more waves of bank-conflict-free bitwise instructions (probe:
+# 2.10-2.13; in kernels 2.2-2.4: the peak assumes 2)
 ISSUE_CLOCKS = 4.44
 SIMD_CLOCKS = 2.24
 
@@ -55,7 +55,7 @@ IN_FMT, ACC_FMT, OUT_FMT = (5, 3), (5, 4), (5, 4)
 # counter reads for a plain 256 MiB device copy (FETCH x2.0, WRITE x1.0); see
 # the profiles/ summaries. Set to None whenever the kernel changes, until the
 # counters are taken again.
-TRAFFIC = (3559.9 * 2.0 + 6272.4 * 1.0) * 1024   # 13.71 MB (split kernel, float32 OFM)
+TRAFFIC = (3556.9 * 2.0 + 6272.0 * 1.0) * 1024   # 13.71 MB (split kernel, float32 OFM)
 
 
 def log(*a):
