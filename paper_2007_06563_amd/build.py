@@ -31,7 +31,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 from paper_2007_06563_amd import variants  # noqa: E402
-from paper_2007_06563_amd.gen import align, asmgen, emit, fp, opt, regalloc  # noqa: E402
+from paper_2007_06563_amd.gen import align, asmgen, banks, emit, fp, opt, regalloc  # noqa: E402
 
 
 def nb(wE, wF):
@@ -478,6 +478,10 @@ LLVM_MC = "/opt/rocm/llvm/bin/llvm-mc"
 # waves per SIMD, which hide a wave's misaligned fetches, and measured up to
 # 5 % slower with the pass's re-encodings and nops; they are left as compiled.
 ALIGN_KERNELS = ("19conv2d_split_kernel", "13muladd_kernel", "14avgpool_kernel", "11pack_kernel")
+# Kernels whose compiled netlists get the VGPR bank pass (gen/banks.py): the
+# fused conv, whose MAC runs with several waves per SIMD, where an
+# instruction reading two sources from one bank costs about twice the time.
+BANK_KERNELS = ("13conv2d_kernel",)
 
 
 def _compile_plain(src, obj):
@@ -518,8 +522,13 @@ def _compile(src, obj, stats=None):
                 if r.returncode != 0:
                     raise RuntimeError(f"device compile failed on {src}:\n{r.stderr[-4000:]}")
                 text = open(asm).read()
+                text, bst = banks.rename_text(text, only=BANK_KERNELS)
+                if bst["blocks"]:
+                    with open(asm, "w") as f:
+                        f.write(text)
                 new, st = align.align_text(text, align.encoding_sizes(asm, LLVM_MC),
                                            only=ALIGN_KERNELS)
+                st.update({k: v for k, v in bst.items() if k.startswith("conflicts")})
                 with open(fixed, "w") as f:
                     f.write(new)
                 c = [LLVM_MC, "-triple=amdgcn-amd-amdhsa", "-mcpu=gfx950", "-filetype=obj",
@@ -552,9 +561,12 @@ def build(jobs=None, verbose=True):
         for f in futs:
             objs.append(f.result())
     if verbose:
-        tot = {k: sum(st[k] for st in stats.values()) for k in ("promoted", "nops", "left")}
+        tot = {k: sum(st.get(k, 0) for st in stats.values())
+               for k in ("promoted", "nops", "left", "conflicts_before", "conflicts_after")}
         print(f"8-byte alignment: {tot['promoted']} VALU instructions re-encoded as VOP3, "
               f"{tot['nops']} s_nop inserted, {tot['left']} short runs left")
+        print(f"VGPR banks: {tot['conflicts_before']} -> {tot['conflicts_after']} instructions "
+              "with two sources in one bank in the renamed blocks")
     tmp = LIB + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=gfx950", "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
