@@ -126,14 +126,15 @@ def _time(fn, reps, stream):
     return e0.elapsed_time(e1) / reps
 
 
+KERNEL_NAME = {1: "fused", 2: "split", 3: "split_compact"}
+
+
 def _conv_ops(d):
-    """(algorithm the library picks, VALU ops per 32-MAC word of that kernel)."""
-    cus = torch.cuda.get_device_properties(0).multi_processor_count
-    P = d.N * hf.conv_out_hw(d)[0] * hf.conv_out_hw(d)[1]
-    chain_waves = ((P + 63) // 64) * ((d.M + 31) // 32)
-    algo = hf.ALGO_SPLIT if chain_waves <= 4 * cus else hf.ALGO_FUSED
+    """(kernel shape the library runs d in, VALU ops per 32-MAC word of that
+    kernel)."""
+    algo = hf.conv2d_algo(d)
     ops = hf.netlist_ops((d.in_fmt.wE, d.in_fmt.wF), (d.acc_fmt.wE, d.acc_fmt.wF), d.round)
-    return algo, (ops["mul"] + ops["accum"] if algo == hf.ALGO_SPLIT else ops["mac"])
+    return algo, (ops["mac"] if algo == hf.ALGO_FUSED else ops["mul"] + ops["accum"])
 
 
 def issue_ceiling(d, algo):
@@ -153,6 +154,12 @@ def issue_ceiling(d, algo):
         G, clocks = ops["mul"] + ops["accum"], taps * ops["accum"] * ISSUE_CLOCKS
         if chain_waves > N_SIMD:  # more chain sets than SIMDs: some run one after another
             clocks *= -(-chain_waves // N_SIMD)
+    elif algo == hf.ALGO_SPLIT_COMPACT:
+        # up to two accumulator/multiplier pairs per SIMD: a SIMD's share of
+        # both netlists, or one accumulator's chain, whichever is longer
+        G = ops["mul"] + ops["accum"]
+        per_simd = -(-chain_waves // N_SIMD)
+        clocks = max(taps * ops["accum"] * ISSUE_CLOCKS, taps * per_simd * G * SIMD_CLOCKS)
     else:
         G = ops["mac"]
         wgs_per_cu = -(-((P + 255) // 256) * ((d.M + 31) // 32) // N_CU)
@@ -286,7 +293,7 @@ def suite(reps, only=None):
             lane_ops = s.macs / 32.0 * G
             print(json.dumps({
                 "workload": label,
-                "kernel": "split" if algo == hf.ALGO_SPLIT else "fused", "ms": ms,
+                "kernel": KERNEL_NAME[algo], "ms": ms,
                 "gmacs": s.macs / (ms * 1e-3) / 1e9, "ops_per_mac_word": G,
                 "roofline": {"bound": "alu", "achieved": lane_ops / (ms * 1e-3) / 1e12,
                              "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
@@ -326,7 +333,7 @@ def suite(reps, only=None):
         total_ms += ms
         print(json.dumps({
             "workload": stack_labels[li],
-            "kernel": "split" if algo == hf.ALGO_SPLIT else "fused", "ms": ms,
+            "kernel": KERNEL_NAME[algo], "ms": ms,
             "gmacs": s.macs / (ms * 1e-3) / 1e9, "ops_per_mac_word": G,
             "roofline": {"bound": "alu", "achieved": s.macs / 32.0 * G / (ms * 1e-3) / 1e12,
                          "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
@@ -406,7 +413,7 @@ def sweep(reps):
                 "gates": {"mac": ops["mac"], "mul": ops["mul"], "accum": ops["accum"],
                           "muladd": ops["muladd"]},
                 "workload": f"conv {s.N}x{s.H}x{s.W}x{s.C} -> {s.M} 3x3 s2 p1",
-                "kernel": "split" if algo == hf.ALGO_SPLIT else "fused", "ms": ms,
+                "kernel": KERNEL_NAME[algo], "ms": ms,
                 "gmacs": s.macs / (ms * 1e-3) / 1e9,
                 "roofline": {"bound": "alu", "achieved": lane_ops / (ms * 1e-3) / 1e12,
                              "peak": PEAK_LANE_OPS / 1e12, "unit": "T VALU-op/s",
@@ -473,11 +480,11 @@ def main():
     s = I.RESNET_CONV_SHAPE
     ifm, w = I.resnet_conv_inputs()
     P = s.N * s.OH * s.OW
-    # the library's automatic choice: split multiply/accumulate waves when the
-    # accumulator waves would leave each SIMD at most one
-    cus = torch.cuda.get_device_properties(dev).multi_processor_count
-    chain_waves = ((P + 63) // 64) * ((s.M + 31) // 32)
-    algo = hf.ALGO_SPLIT if chain_waves <= 4 * cus else hf.ALGO_FUSED
+    # the library's automatic choice of kernel shape (for this layer: split
+    # multiply/accumulate waves, its accumulator waves leaving each SIMD at
+    # most one)
+    algo = hf.conv2d_algo(hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad,
+                                       IN_FMT, ACC_FMT, OUT_FMT, hf.ACT_NONE, hf.ALGO_AUTO))
     # the last (here: only) layer writes float32 directly: the unpack is fused
     # into the convolution's epilogue
     d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, IN_FMT, ACC_FMT,
@@ -528,7 +535,7 @@ def main():
 
     macs = s.macs
     ops = hf.netlist_ops(IN_FMT, ACC_FMT)
-    G = ops["mul"] + ops["accum"] if algo == hf.ALGO_SPLIT else ops["mac"]
+    G = ops["mac"] if algo == hf.ALGO_FUSED else ops["mul"] + ops["accum"]
     lane_ops = macs / 32.0 * G          # 32 MACs per 32-bit word operation
     achieved = lane_ops / (conv_ms * 1e-3)
     ceiling = issue_ceiling(d, algo)
@@ -561,7 +568,8 @@ def main():
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": PEAK_LANE_OPS / 1e12,
                      "unit": "T VALU-op/s (32-bit bitwise, one op = 32 gates)",
                      "frac": achieved / PEAK_LANE_OPS, "traffic": TRAFFIC,
-                     "kernel": "conv2d_split_kernel" if algo == hf.ALGO_SPLIT else "conv2d_kernel",
+                     "kernel": {1: "conv2d_kernel", 2: "conv2d_split_kernel",
+                                3: "conv2d_split_compact_kernel"}[algo],
                      "ops_per_mac_word": G,
                      "kernel_ms": conv_ms,
                      "issue_ceiling": ceiling},

@@ -82,12 +82,21 @@ enum { HOBFLOPS_SRC_F32 = 0, HOBFLOPS_SRC_CODE_U32 = 1 };
 enum { HOBFLOPS_ROUND_NEAREST_EVEN = 0, HOBFLOPS_ROUND_TOWARD_ZERO = 1 };
 enum { HOBFLOPS_ORDER_KY_KX_C = 0 };
 enum { HOBFLOPS_ACT_NONE = 0, HOBFLOPS_ACT_RELU = 1 };
-/* Kernel shape of hobflops_conv2d (results are identical for all three):
- * AUTO picks SPLIT when the launch has at most one accumulator wave per SIMD
- * of the device and FUSED otherwise; FUSED runs multiplier and adder on the
- * same wave; SPLIT runs them on separate waves of the same CU so that a
- * launch with few accumulator chains can still fill the VALU. */
-enum { HOBFLOPS_ALGO_AUTO = 0, HOBFLOPS_ALGO_FUSED = 1, HOBFLOPS_ALGO_SPLIT = 2 };
+/* Kernel shape of hobflops_conv2d (results are identical for all four):
+ * FUSED runs multiplier and adder on the same wave; SPLIT runs them on
+ * separate waves of the same CU (one accumulator/multiplier pair per SIMD) so
+ * that a launch with few accumulator chains can still fill the VALU;
+ * SPLIT_COMPACT is SPLIT in a form of which two workgroups share a CU (two
+ * pairs per SIMD, two products per hand-over). AUTO picks SPLIT when the
+ * launch has at most one accumulator wave (64 positions of one 32-kernel
+ * tile) per SIMD of the device, SPLIT_COMPACT (else SPLIT) when it has at most
+ * two, and FUSED otherwise. */
+enum {
+  HOBFLOPS_ALGO_AUTO = 0,
+  HOBFLOPS_ALGO_FUSED = 1,
+  HOBFLOPS_ALGO_SPLIT = 2,
+  HOBFLOPS_ALGO_SPLIT_COMPACT = 3
+};
 /* What hobflops_conv2d writes to ofm: PL32 planes of out_fmt (the next
  * layer's input, the default), or with the unpack fused into the epilogue
  * (the last layer, paper Sec. 3.4), one value per element, row-major
@@ -153,8 +162,9 @@ int hobflops_unpack(const uint32_t* planes, int64_t rows, int64_t len, hobflops_
  *   acc_fmt.wF = in_fmt.wF + 1 this is the paper's "single" MAC type, with
  *   2 * in_fmt.wF + 1 its "extended" type, whose products are exact (Table 3).
  *   round: HOBFLOPS_ROUND_* for every mul, add and the final convert; order
- *   must be HOBFLOPS_ORDER_KY_KX_C. algo SPLIT returns HOBFLOPS_EUNSUPPORTED
- *   for a variant generated without the split kernel; AUTO then runs FUSED. */
+ *   must be HOBFLOPS_ORDER_KY_KX_C. algo SPLIT (SPLIT_COMPACT) returns
+ *   HOBFLOPS_EUNSUPPORTED for a variant generated without that kernel (its
+ *   netlists do not fit the registers); AUTO then picks among the others. */
 typedef struct {
   int N, H, W, C, M, KH, KW, stride, pad;
   hobflops_fmt in_fmt, acc_fmt, out_fmt;
@@ -167,8 +177,16 @@ int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
                     const hobflops_conv_desc* d, void* stream);
 
 /* 1 if hobflops_conv2d has a kernel for d's formats, activation, rounding
- * mode and (for HOBFLOPS_ALGO_SPLIT) kernel shape, else 0. */
+ * mode and (for HOBFLOPS_ALGO_SPLIT and _SPLIT_COMPACT) kernel shape, else 0. */
 int hobflops_conv2d_supported(const hobflops_conv_desc* d);
+
+/* The kernel shape hobflops_conv2d runs d in (HOBFLOPS_ALGO_FUSED, _SPLIT or
+ * _SPLIT_COMPACT): d->algo itself, or for HOBFLOPS_ALGO_AUTO the shape AUTO
+ * picks on the current device. Returns that value (>= 1), or a negative
+ * status: HOBFLOPS_EINVAL for a bad descriptor, HOBFLOPS_EUNSUPPORTED where
+ * hobflops_conv2d_supported is 0, HOBFLOPS_EHIP if AUTO cannot query the
+ * device. Launches nothing. */
+int hobflops_conv2d_algo(const hobflops_conv_desc* d);
 
 /* Element-wise r = add(widen(c), mul(a, b)) over n elements of flat PL32
  * tensors (rows 1, len n): a, b, c in in_fmt, r in acc_fmt (same wE,
@@ -218,7 +236,8 @@ int hobflops_avgpool_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, hobflo
 int hobflops_avgpool_netlist_ops(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, hobflops_fmt out_fmt,
                                  int round, int* accum_ops, int* scale_ops);
 
-/* Diagnostics of the split convolution kernel (HOBFLOPS_ALGO_SPLIT). Its
+/* Diagnostics of the split convolution kernel (HOBFLOPS_ALGO_SPLIT and
+ * _SPLIT_COMPACT). Its
  * multiplier and accumulator waves hand products over through counters in
  * LDS; every wait for a counter sleeps at most a bounded number of times
  * (about 64 clocks each), so that a counter that never came would end the

@@ -10,6 +10,7 @@ import concurrent.futures as cf
 import hashlib
 import json
 import os
+import re
 import shlex
 import shutil
 import subprocess
@@ -212,12 +213,32 @@ def split_batches(naccp, slots=None):
     return [K for K in SPLIT_BATCHES if slots * K * 256 * naccp * 4 <= 144 * 1024]
 
 
-def split_asm(wE, wi, wa, rnd, cache):
+# The compact form of the split kernel: two workgroups per CU, i.e. two
+# accumulator/multiplier wave pairs per SIMD, for launches with between one
+# and two chains per SIMD. That needs at most 128 VGPRs a wave (the asm
+# blocks end at v128) and an LDS product ring of at most 80 KiB, hence two
+# products per hand-over.
+COMPACT_TOP, COMPACT_BATCH = 128, 2
+COMPACT_BASES = ((32, 48), (24, 48), (32, 56), (24, 40), (32, 40))
+# Variants whose compact kernel the compiler could only fit by spilling
+# registers to scratch (found by build(), which then rebuilds them without
+# the compact form: a spilling kernel would defeat its purpose).
+COMPACT_SPILLS = os.path.join(GEN, "compact_spills.json")
+
+
+def _compact_excluded():
+    return set(json.load(open(COMPACT_SPILLS))) if os.path.exists(COMPACT_SPILLS) else set()
+
+
+def split_asm(wE, wi, wa, rnd, cache, compact=False):
     """The split kernel's assembly for one variant (with "batch", the products
     per hand-over), or None when the two netlists do not fit the registers the
-    asm blocks may use at any batch size."""
+    asm blocks may use at any batch size. compact: the two-workgroups-per-CU
+    form (blocks below v128, two products per hand-over)."""
     key = (f"split_e{wE}m{wi}_a{wa}{variants._sfx(rnd)}"
            f"_s{SPLIT_SLOTS}_{SPLIT_SCHEDULE}_{SPLIT_SYNC}_k" + "".join(map(str, SPLIT_BATCHES)))
+    if compact:
+        key = f"split_compact_e{wE}m{wi}_a{wa}{variants._sfx(rnd)}_t{COMPACT_TOP}_k{COMPACT_BATCH}"
     if key not in cache:
         r = variants.RND_NAME[rnd]
         nin, nacc = nb(wE, wi), nb(wE, wa)
@@ -230,13 +251,17 @@ def split_asm(wE, wi, wa, rnd, cache):
         # accumulator's role keeps only a few values of the compiler's, so its
         # window may start as low as v32; the multiplier's stays at v80 or up.
         bases = ((96, 96), (80, 80), (48, 80), (32, 80))
-        for K in split_batches(asmgen.pad4(nacc)):
+        batches = split_batches(asmgen.pad4(nacc))
+        top = None
+        if compact:
+            bases, batches, top = COMPACT_BASES, [COMPACT_BATCH], COMPACT_TOP
+        for K in batches:
             best = None
             for base, mul_base in bases:
                 try:
                     text, stats = asmgen.split_functions(acc_c, prod_c, nin, nacc, K,
                                                          SPLIT_SLOTS, SPLIT_SCHEDULE, SPLIT_SYNC,
-                                                         base=base, mul_base=mul_base)
+                                                         base=base, mul_base=mul_base, top=top)
                 except regalloc.AllocError as e:
                     cache[key] = {"text": None, "stats": {"unavailable": str(e)}}
                     continue
@@ -253,6 +278,7 @@ def split_asm(wE, wi, wa, rnd, cache):
 
 def generate(verbose=True):
     os.makedirs(GEN, exist_ok=True)
+    compact_excluded = _compact_excluded()
     digest = _gen_sources_digest()
     cache_path = os.path.join(GEN, "netlists.json")
     cache = {}
@@ -296,6 +322,9 @@ def generate(verbose=True):
         accum, accum_e = netlist("accum", (wE, wa), rnd, cache)
         sp = split_asm(wE, wi, wa, rnd, cache)
         split_text = sp["text"] if sp else ""
+        spc = (split_asm(wE, wi, wa, rnd, cache, compact=True)
+               if sp and f"conv_{tag}" not in compact_excluded else None)
+        compact_text = f"namespace compact {{\n{spc['text']}}}  // namespace compact\n" if spc else ""
         split_members = """  static constexpr int kBatch = {batch};
   static constexpr const int* kAccSlot = conv_{tag}::kAccSlot;
   static constexpr const int* kProdSlot = conv_{tag}::kProdSlot;
@@ -317,11 +346,39 @@ def generate(verbose=True):
     conv_{tag}::product_batch(xw, c, wrow, entry);
   }}
 """.format(batch=sp["batch"], tag=tag) if sp else ""
-        split_launch = f"""  if (algo == kAlgoSplit)
+        # the compact form: the same kernel body with the compact asm blocks
+        compact_struct = """struct VC : V {{
+  static constexpr int kBatch = {batch};
+  static constexpr const int* kAccSlot = compact::kAccSlot;
+  static constexpr const int* kProdSlot = compact::kProdSlot;
+  static constexpr const int* kWSlot = compact::kWSlot;
+  static constexpr int kSlots = compact::kSlots;
+  static constexpr bool kPairs = compact::kPairs;
+  static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[(NACC + 3) & ~3],
+                                                    const lds_u32* e0, const lds_u32* e1,
+                                                    const lds_u32* e2, const lds_u32* fl,
+                                                    int nb, uint32_t cap, uint32_t& gave) {{
+    compact::accum_loop(acc, e0, e1, e2, fl, nb, cap, gave);
+  }}
+  static __device__ __forceinline__ void product_step(const uint32_t (&xw)[NIN], int c,
+                                                      const lds_u32* wrow, lds_u32* entry) {{
+    compact::product_step(xw, c, wrow, entry);
+  }}
+  static __device__ __forceinline__ void product_batch(const uint32_t (&xw)[NIN], int c,
+                                                       const lds_u32* wrow, lds_u32* entry) {{
+    compact::product_batch(xw, c, wrow, entry);
+  }}
+}};
+""".format(batch=spc["batch"]) if spc else ""
+        split_launch = (f"""  if (algo == kAlgoSplitCompact)
+    hipLaunchKernelGGL(conv2d_split_compact_kernel<conv_{tag}::VC>, grid, dim3(2 * kConvBlock), 0,
+                       stream, ifm, w, ofm, p);
+  else
+""" if spc else "") + (f"""  if (algo == kAlgoSplit)
     hipLaunchKernelGGL(conv2d_split_kernel<conv_{tag}::V>, grid, dim3(2 * kConvBlock), 0, stream,
                        ifm, w, ofm, p);
   else
-""" if sp else ""
+""" if sp else "")
         src = f"""// Generated: convolution variant {tag}. Do not edit.
 #include "kernels.hpp"
 #include "registry.hpp"
@@ -332,6 +389,7 @@ namespace conv_{tag} {{
 {cache[prod]['text']}
 {cache[accum]['text']}
 {split_text}
+{compact_text}
 struct V {{
   static constexpr int NIN = {nb(wE, wi)}, NACC = {nb(wE, wa)}, NOUT = {nb(wE, wo)};
   static constexpr int wE = {wE}, wF_OUT = {wo};
@@ -346,7 +404,7 @@ struct V {{
     {epi}(acc, out);
   }}
 }};
-}}  // namespace conv_{tag}
+{compact_struct}}}  // namespace conv_{tag}
 hipError_t launch_conv_{tag}(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
                               const ConvParams& p, int algo, hipStream_t stream) {{
   dim3 grid((unsigned)((p.P + kConvBlock - 1) / kConvBlock), (unsigned)p.MT);
@@ -356,7 +414,8 @@ hipError_t launch_conv_{tag}(const uint32_t* ifm, const uint32_t* w, uint32_t* o
 }}  // namespace hobflops
 """
         files.append((f"conv_{tag}.hip", src))
-        reg_conv.append((v, tag, mac_e["ops"], prod_e["ops"], accum_e["ops"], 1 if sp else 0))
+        reg_conv.append((v, tag, mac_e["ops"], prod_e["ops"], accum_e["ops"], 1 if sp else 0,
+                         1 if spc else 0))
     for v in variants.MULADD_VARIANTS:
         wE, wi, wa, rnd = v
         tag = variants.muladd_tag(v)
@@ -432,9 +491,9 @@ hipError_t launch_pool_{tag}(const uint32_t* in, uint32_t* out, const PoolParams
         reg.append(f"hipError_t launch_pool_{tag}(const uint32_t*, uint32_t*, const PoolParams&, "
                    f"hipStream_t);")
     reg.append("const ConvVariant kConvVariants[] = {")
-    for v, tag, ops, pops, aops, has_split in reg_conv:
-        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {v[4]}, {v[5]}, {has_split}, {ops}, "
-                   f"{pops}, {aops}, launch_conv_{tag}}},")
+    for v, tag, ops, pops, aops, has_split, has_compact in reg_conv:
+        reg.append(f"  {{{v[0]}, {v[1]}, {v[2]}, {v[3]}, {v[4]}, {v[5]}, {has_split}, "
+                   f"{has_compact}, {ops}, {pops}, {aops}, launch_conv_{tag}}},")
     reg.append("};")
     reg.append(f"const int kNumConvVariants = {len(reg_conv)};")
     reg.append("const MuladdVariant kMuladdVariants[] = {")
@@ -492,6 +551,22 @@ def _compile_plain(src, obj):
     return obj
 
 
+def _compact_spills(text):
+    """Variant tags whose compact split kernel uses scratch (spilled VGPRs),
+    from the kernel descriptors of one source's device assembly."""
+    out = []
+    for m in re.finditer(r"\.amdhsa_kernel (\S+)\n((?:\s+\.amdhsa\w+ [^\n]*\n)+)", text):
+        name, body = m.group(1), m.group(2)
+        k = name.find("27conv2d_split_compact_kernelINS_")
+        seg = re.search(r"\.amdhsa_private_segment_fixed_size (\d+)", body)
+        if k < 0 or not seg or int(seg.group(1)) == 0:
+            continue
+        rest = name[k + len("27conv2d_split_compact_kernelINS_"):]
+        n = re.match(r"\d+", rest)
+        out.append(rest[n.end():n.end() + int(n.group(0))])
+    return out
+
+
 def _compile(src, obj, stats=None):
     """hipcc -c, with the device code taken through assembly text so that
     gen/align.py can keep its 8-byte instructions 8-byte aligned: the
@@ -522,6 +597,7 @@ def _compile(src, obj, stats=None):
                 if r.returncode != 0:
                     raise RuntimeError(f"device compile failed on {src}:\n{r.stderr[-4000:]}")
                 text = open(asm).read()
+                spills = _compact_spills(text)
                 text, bst = banks.rename_text(text, only=BANK_KERNELS)
                 if bst["blocks"]:
                     with open(asm, "w") as f:
@@ -529,6 +605,7 @@ def _compile(src, obj, stats=None):
                 new, st = align.align_text(text, align.encoding_sizes(asm, LLVM_MC),
                                            only=ALIGN_KERNELS)
                 st.update({k: v for k, v in bst.items() if k.startswith("conflicts")})
+                st["compact_spills"] = spills
                 with open(fixed, "w") as f:
                     f.write(new)
                 c = [LLVM_MC, "-triple=amdgcn-amd-amdhsa", "-mcpu=gfx950", "-filetype=obj",
@@ -552,14 +629,24 @@ def build(jobs=None, verbose=True):
     srcs = [os.path.join(HERE, "csrc", "abi.hip"), os.path.join(HERE, "csrc", "pack.hip")] + gen_files
     os.makedirs(OBJ, exist_ok=True)
     jobs = jobs or min(16, os.cpu_count() or 4)
-    objs, stats = [], {}
-    with cf.ThreadPoolExecutor(jobs) as ex:
-        futs = []
-        for s in srcs:
-            o = os.path.join(OBJ, os.path.basename(s) + ".o")
-            futs.append(ex.submit(_compile, s, o, stats))
-        for f in futs:
-            objs.append(f.result())
+    stats = {}
+
+    def compile_all(files):
+        with cf.ThreadPoolExecutor(jobs) as ex:
+            futs = [ex.submit(_compile, f, os.path.join(OBJ, os.path.basename(f) + ".o"), stats)
+                    for f in files]
+            return [f.result() for f in futs]
+
+    objs = compile_all(srcs)
+    spilled = sorted({t for st in stats.values() for t in st.get("compact_spills", [])})
+    if spilled:
+        # drop the compact form of those variants and compile their sources again
+        json.dump(sorted(_compact_excluded() | set(spilled)), open(COMPACT_SPILLS, "w"))
+        if verbose:
+            print("compact split kernel spills registers, left out:", ", ".join(spilled))
+        generate(verbose=False)
+        compile_all([os.path.join(GEN, t + ".hip") for t in spilled] +
+                    [os.path.join(GEN, "registry.hip")])
     if verbose:
         tot = {k: sum(st.get(k, 0) for st in stats.values())
                for k in ("promoted", "nops", "left", "conflicts_before", "conflicts_after")}

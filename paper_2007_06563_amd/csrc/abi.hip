@@ -139,7 +139,7 @@ int conv_check(const hobflops_conv_desc* d) {
   if (d->act != HOBFLOPS_ACT_NONE && d->act != HOBFLOPS_ACT_RELU) return HOBFLOPS_EINVAL;
   if (!round_ok(d->round) || d->order != HOBFLOPS_ORDER_KY_KX_C) return HOBFLOPS_EINVAL;
   if (d->algo != HOBFLOPS_ALGO_AUTO && d->algo != HOBFLOPS_ALGO_FUSED &&
-      d->algo != HOBFLOPS_ALGO_SPLIT)
+      d->algo != HOBFLOPS_ALGO_SPLIT && d->algo != HOBFLOPS_ALGO_SPLIT_COMPACT)
     return HOBFLOPS_EINVAL;
   if (d->ofm_kind != HOBFLOPS_OFM_PLANES && d->ofm_kind != HOBFLOPS_OFM_F32 &&
       d->ofm_kind != HOBFLOPS_OFM_CODE_U32)
@@ -206,10 +206,53 @@ int hobflops_unpack(const uint32_t* planes, int64_t rows, int64_t len, hobflops_
   return hip_status(launch_unpack(planes, rows, len, f.wE, f.wF, kind, dst, (hipStream_t)stream));
 }
 
+// The kernel shape a conv runs in: d->algo, or for AUTO the choice below,
+// made from the launch's chain waves (one accumulator wave per 64 positions
+// and 32-kernel tile). Up to one per SIMD: the split kernel, one wave pair per
+// SIMD. Up to two: its compact form, two pairs per SIMD in one round of
+// workgroups (or the split kernel in two rounds where the compact form was
+// not generated). More: the fused kernel, whose waves fill the SIMDs by
+// themselves.
+static int resolve_algo(const hobflops_conv_desc* d, const ConvVariant* v, int* algo) {
+  *algo = d->algo;
+  if (d->algo != HOBFLOPS_ALGO_AUTO) return HOBFLOPS_OK;
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return hip_status(e);
+  const int64_t OH = (d->H + 2 * (int64_t)d->pad - d->KH) / d->stride + 1;
+  const int64_t OW = (d->W + 2 * (int64_t)d->pad - d->KW) / d->stride + 1;
+  const int64_t P = (int64_t)d->N * OH * OW;
+  const int64_t chain_waves = (P + 63) / 64 * ((d->M + 31) / 32);
+  const int64_t simds = 4 * (int64_t)cus;
+  if (chain_waves <= simds && v->has_split)
+    *algo = HOBFLOPS_ALGO_SPLIT;
+  else if (chain_waves <= 2 * simds && v->has_compact)
+    *algo = HOBFLOPS_ALGO_SPLIT_COMPACT;
+  else if (chain_waves <= 2 * simds && v->has_split)
+    *algo = HOBFLOPS_ALGO_SPLIT;
+  else
+    *algo = HOBFLOPS_ALGO_FUSED;
+  return HOBFLOPS_OK;
+}
+
+int hobflops_conv2d_algo(const hobflops_conv_desc* d) {
+  const int st = conv_check(d);
+  if (st != HOBFLOPS_OK) return st;
+  const ConvVariant* v = find_conv(d);
+  if (!v || (d->algo == HOBFLOPS_ALGO_SPLIT && !v->has_split) ||
+      (d->algo == HOBFLOPS_ALGO_SPLIT_COMPACT && !v->has_compact))
+    return HOBFLOPS_EUNSUPPORTED;
+  int algo = 0;
+  const int st2 = resolve_algo(d, v, &algo);
+  return st2 != HOBFLOPS_OK ? st2 : algo;
+}
+
 int hobflops_conv2d_supported(const hobflops_conv_desc* d) {
   if (conv_check(d) != HOBFLOPS_OK) return 0;
   const ConvVariant* v = find_conv(d);
-  return v != nullptr && (d->algo != HOBFLOPS_ALGO_SPLIT || v->has_split);
+  return v != nullptr && (d->algo != HOBFLOPS_ALGO_SPLIT || v->has_split) &&
+         (d->algo != HOBFLOPS_ALGO_SPLIT_COMPACT || v->has_compact);
 }
 
 int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
@@ -219,7 +262,9 @@ int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
   if (!ifm || !w || !ofm) return HOBFLOPS_EINVAL;
   if (!aligned(ifm) || !aligned(w) || !aligned(ofm)) return HOBFLOPS_EALIGN;
   const ConvVariant* v = find_conv(d);
-  if (!v || (d->algo == HOBFLOPS_ALGO_SPLIT && !v->has_split)) return HOBFLOPS_EUNSUPPORTED;
+  if (!v || (d->algo == HOBFLOPS_ALGO_SPLIT && !v->has_split) ||
+      (d->algo == HOBFLOPS_ALGO_SPLIT_COMPACT && !v->has_compact))
+    return HOBFLOPS_EUNSUPPORTED;
   ConvParams p;
   p.N = d->N;
   p.H = d->H;
@@ -242,20 +287,15 @@ int hobflops_conv2d(const uint32_t* ifm, const uint32_t* w, uint32_t* ofm,
     const hipError_t e = wait_fail_word(&p.wait_fail);
     if (e != hipSuccess) return hip_status(e);
   }
-  int algo = d->algo;
-  if (algo == HOBFLOPS_ALGO_AUTO) {
-    // one accumulator wave per 64 positions and m-tile; split when they would
-    // leave the SIMDs of the device at most one each
-    int dev = 0, cus = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e != hipSuccess) return hip_status(e);
-    const int64_t chain_waves = (int64_t)((p.P + 63) / 64) * p.MT;
-    algo = chain_waves <= 4 * (int64_t)cus && v->has_split ? HOBFLOPS_ALGO_SPLIT
-                                                           : HOBFLOPS_ALGO_FUSED;
+  int algo = 0;
+  {
+    const int st2 = resolve_algo(d, v, &algo);
+    if (st2 != HOBFLOPS_OK) return st2;
   }
-  return hip_status(v->launch(ifm, w, ofm, p, algo == HOBFLOPS_ALGO_SPLIT ? kAlgoSplit : kAlgoFused,
-                              (hipStream_t)stream));
+  const int kalgo = algo == HOBFLOPS_ALGO_SPLIT           ? kAlgoSplit
+                    : algo == HOBFLOPS_ALGO_SPLIT_COMPACT ? kAlgoSplitCompact
+                                                          : kAlgoFused;
+  return hip_status(v->launch(ifm, w, ofm, p, kalgo, (hipStream_t)stream));
 }
 
 int hobflops_muladd_supported(hobflops_fmt in_fmt, hobflops_fmt acc_fmt, int round) {

@@ -126,7 +126,7 @@ constexpr int kConvBlock = 256;  // positions per workgroup: four wave64s
 constexpr uint32_t kSpinCap = 1u << 20;
 
 // Kernel shapes of the convolution (hobflops_conv_desc.algo).
-constexpr int kAlgoAuto = 0, kAlgoFused = 1, kAlgoSplit = 2;
+constexpr int kAlgoAuto = 0, kAlgoFused = 1, kAlgoSplit = 2, kAlgoSplitCompact = 3;
 
 
 // MCMK convolution (paper Sec. 3.4). One lane owns one output position and
@@ -321,9 +321,9 @@ __global__ __launch_bounds__(kConvBlock) void conv2d_kernel(const uint32_t* __re
 // b-2, before a barrier, and is read only after the barrier that ends b.
 // Every wave reaches every barrier, so the loop cannot deadlock.
 template <class V>
-__global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
-    const uint32_t* __restrict__ ifm, const uint32_t* __restrict__ w, uint32_t* __restrict__ ofm,
-    ConvParams p) {
+__device__ __forceinline__ void conv2d_split_body(const uint32_t* __restrict__ ifm,
+                                                  const uint32_t* __restrict__ w,
+                                                  uint32_t* __restrict__ ofm, const ConvParams& p) {
   constexpr int NIN = V::NIN, NACC = V::NACC, NOUT = V::NOUT;
   constexpr int NINP = (NIN + 3) & ~3;    // weight row stride in LDS (16-byte aligned)
   constexpr int NACCP = (NACC + 3) & ~3;  // product entry per lane (16-byte aligned)
@@ -576,6 +576,28 @@ __global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
   for (int bb = 0; bb < NACC; ++bb) planes[bb] = acc[V::kAccSlot[bb]];
   V::epi(planes, out);
   store_ofm<NOUT, V::wE, V::wF_OUT>(out, ofm, pos, mt, p);
+}
+
+// The split kernel with one workgroup per CU: one accumulator/multiplier wave
+// pair per SIMD, the netlists' registers anywhere up to v255 and up to four
+// products per hand-over. For launches with at most one chain wave per SIMD.
+template <class V>
+__global__ __launch_bounds__(2 * kConvBlock) void conv2d_split_kernel(
+    const uint32_t* __restrict__ ifm, const uint32_t* __restrict__ w, uint32_t* __restrict__ ofm,
+    ConvParams p) {
+  conv2d_split_body<V>(ifm, w, ofm, p);
+}
+
+// The compact form: at most 128 VGPRs a wave (the variant's asm blocks end at
+// v128) and an LDS ring of two products per hand-over, so that two workgroups
+// share a CU and each SIMD runs two wave pairs. For launches with between one
+// and two chain waves per SIMD, where the one-workgroup form would need a
+// second round of workgroups.
+template <class V>
+__global__ __launch_bounds__(2 * kConvBlock) __attribute__((amdgpu_waves_per_eu(4)))
+void conv2d_split_compact_kernel(const uint32_t* __restrict__ ifm, const uint32_t* __restrict__ w,
+                                 uint32_t* __restrict__ ofm, ConvParams p) {
+  conv2d_split_body<V>(ifm, w, ofm, p);
 }
 
 // Element-wise r = a*b + c (multiply rounded, then add rounded) on flat PL32

@@ -17,6 +17,7 @@ struct ConvVariant {
   int wE, wF_in, wF_acc, wF_out, act;
   int round;      // HOBFLOPS_ROUND_*
   int has_split;  // the split kernel was generated (its netlists fit the registers)
+  int has_compact;  // ... and its compact form (two workgroups per CU)
   int mac_ops;    // VALU bitwise instructions of one fused multiply-add step
   int mul_ops;    // ... of the multiplier alone (split kernel, multiplier waves)
   int accum_ops;  // ... of the accumulating adder alone (split kernel, adder waves)

@@ -66,7 +66,7 @@ def _asm_string(lines):
 
 
 def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sync="barrier",
-                    base=None, mul_base=None):
+                    base=None, mul_base=None, top=None):
     """C++ text (inside a variant's namespace) of the two asm functions and
     their slot tables, plus allocation statistics.
 
@@ -100,6 +100,7 @@ def split_functions(accum_C, prod_C, nin, nacc, K, slots=2, schedule="batch", sy
     # (the roles are separate branches, so their windows may differ)
     BASE = globals()["BASE"] if base is None else base
     MUL_BASE = BASE if mul_base is None else mul_base
+    TOP = globals()["TOP"] if top is None else top  # one past the last register the blocks use
     ninp, naccp = pad4(nin), pad4(nacc)
     kstride = naccp // 4
     A = list(range(BASE, BASE + naccp))
@@ -257,7 +258,7 @@ static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], cons
 }}
 """
         mul_fn, stats = _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot,
-                                       entry_bytes, st_acc, MUL_BASE)
+                                       entry_bytes, st_acc, MUL_BASE, TOP)
         return accum_fn + mul_fn, stats
 
     carried = [("r", 0, 0)] if schedule == "prefetch" else []
@@ -309,12 +310,12 @@ static __device__ __forceinline__ void accum_loop(uint32_t (&acc)[{naccp}], cons
 }}
 """
     mul_fn, stats = _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot,
-                                   entry_bytes, st_acc, MUL_BASE)
+                                   entry_bytes, st_acc, MUL_BASE, TOP)
     return accum_fn + mul_fn, stats
 
 
 def _mul_functions(prod_C, nin, nacc, K, ninp, naccp, kstride, prod_slot, entry_bytes, st_acc,
-                   BASE=BASE):
+                   BASE=BASE, TOP=TOP):
     """The multiplier role's asm functions (the same for both sync modes)."""
     # ---- multiplier role: product planes go to the P block in slot order
     # (plane b at word prod_slot[b]), so a product is stored with 16-byte

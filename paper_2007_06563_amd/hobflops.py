@@ -17,7 +17,7 @@ _lib = None
 SRC_F32, SRC_CODE_U32 = 0, 1
 ACT_NONE, ACT_RELU = 0, 1
 ROUND_NEAREST_EVEN, ROUND_TOWARD_ZERO, ORDER_KY_KX_C = 0, 1, 0
-ALGO_AUTO, ALGO_FUSED, ALGO_SPLIT = 0, 1, 2
+ALGO_AUTO, ALGO_FUSED, ALGO_SPLIT, ALGO_SPLIT_COMPACT = 0, 1, 2, 3
 OFM_PLANES, OFM_F32, OFM_CODE = 0, 1, 2
 
 
@@ -50,7 +50,7 @@ class PackJob(ctypes.Structure):
 
 EXPORTS = ("hobflops_plane_words", "hobflops_pack", "hobflops_pack_batch", "hobflops_unpack",
            "hobflops_conv2d",
-           "hobflops_conv2d_supported", "hobflops_muladd", "hobflops_muladd_supported",
+           "hobflops_conv2d_supported", "hobflops_conv2d_algo", "hobflops_muladd", "hobflops_muladd_supported",
            "hobflops_netlist_ops", "hobflops_avgpool", "hobflops_avgpool_supported",
            "hobflops_avgpool_netlist_ops", "hobflops_wait_failures", "hobflops_set_wait_limit",
            "hobflops_get_wait_limit", "hobflops_status_string")
@@ -71,6 +71,7 @@ def lib():
         L.hobflops_unpack.argtypes = [vp, i64, i64, Fmt, ci, vp, vp]
         L.hobflops_conv2d.argtypes = [vp, vp, vp, ctypes.POINTER(ConvDesc), vp]
         L.hobflops_conv2d_supported.argtypes = [ctypes.POINTER(ConvDesc)]
+        L.hobflops_conv2d_algo.argtypes = [ctypes.POINTER(ConvDesc)]
         L.hobflops_muladd.argtypes = [vp, vp, vp, vp, i64, Fmt, Fmt, ci, vp]
         L.hobflops_muladd_supported.argtypes = [Fmt, Fmt, ci]
         L.hobflops_netlist_ops.argtypes = [Fmt, Fmt, ci] + [ctypes.POINTER(ci)] * 4
@@ -233,6 +234,15 @@ def conv2d(ifm, w, d, out=None):
 
 def conv2d_supported(d):
     return bool(lib().hobflops_conv2d_supported(ctypes.byref(d)))
+
+
+def conv2d_algo(d):
+    """The kernel shape (ALGO_FUSED, ALGO_SPLIT or ALGO_SPLIT_COMPACT) conv2d
+    runs d in: d.algo, or what AUTO picks on the current device."""
+    rc = lib().hobflops_conv2d_algo(ctypes.byref(d))
+    if rc < 0:
+        _check(rc)
+    return rc
 
 
 def muladd(a, b, c, n, in_fmt, acc_fmt, out=None, round=ROUND_NEAREST_EVEN):

@@ -65,7 +65,7 @@ def test_conv_rejects_bad_descriptors(hf, bad):
 
 
 def test_conv_rejects_round_order_and_algo(hf):
-    for field, value in (("round", 2), ("round", -1), ("order", 2), ("algo", 3), ("algo", -1),
+    for field, value in (("round", 2), ("round", -1), ("order", 2), ("algo", 4), ("algo", -1),
                          ("ofm_kind", 3), ("ofm_kind", -1)):
         d = desc(hf)
         setattr(d, field, value)
@@ -96,11 +96,34 @@ def test_split_kernel_availability(hf):
         assert hf.conv2d_supported(desc(hf, **wide, algo=algo))
     assert hf.netlist_ops((5, 10), (5, 21))["mul"] > 0
     missing = dict(in_fmt=(6, 3), acc_fmt=(6, 4), out_fmt=(6, 4))  # not generated
-    for algo in (hf.ALGO_FUSED, hf.ALGO_AUTO, hf.ALGO_SPLIT):
+    for algo in (hf.ALGO_FUSED, hf.ALGO_AUTO, hf.ALGO_SPLIT, hf.ALGO_SPLIT_COMPACT):
         assert not hf.conv2d_supported(desc(hf, **missing, algo=algo))
         d = desc(hf, **missing, algo=algo)
         assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -2
     assert hf.conv2d_supported(desc(hf, algo=hf.ALGO_SPLIT))
+    # the compact form (two workgroups per CU) exists where the netlists fit
+    # 128 VGPRs: the bench format, not the widest extended type
+    assert hf.conv2d_supported(desc(hf, algo=hf.ALGO_SPLIT_COMPACT))
+    assert not hf.conv2d_supported(desc(hf, **wide, algo=hf.ALGO_SPLIT_COMPACT))
+    d = desc(hf, **wide, algo=hf.ALGO_SPLIT_COMPACT)
+    assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -2
+    d = desc(hf, algo=4)  # no such kernel shape
+    assert hf.lib().hobflops_conv2d(FAKE, FAKE, FAKE, ctypes.byref(d), None) == -1
+
+
+def test_conv_algo_query(hf):
+    """hobflops_conv2d_algo reports an explicit kernel shape as given (no
+    device needed), refuses what conv2d would refuse, and resolves AUTO on a
+    device (without one it reports the HIP error)."""
+    for algo in (hf.ALGO_FUSED, hf.ALGO_SPLIT, hf.ALGO_SPLIT_COMPACT):
+        assert hf.conv2d_algo(desc(hf, algo=algo)) == algo
+    wide = dict(in_fmt=(5, 10), acc_fmt=(5, 21), out_fmt=(5, 21))
+    assert hf.lib().hobflops_conv2d_algo(ctypes.byref(
+        desc(hf, **wide, algo=hf.ALGO_SPLIT_COMPACT))) == -2
+    assert hf.lib().hobflops_conv2d_algo(ctypes.byref(desc(hf, algo=4))) == -1
+    assert hf.lib().hobflops_conv2d_algo(None) == -1
+    rc = hf.lib().hobflops_conv2d_algo(ctypes.byref(desc(hf)))  # AUTO
+    assert rc in (hf.ALGO_FUSED, hf.ALGO_SPLIT, hf.ALGO_SPLIT_COMPACT, -4)
 
 
 def test_pack_unpack_argument_checks(hf):

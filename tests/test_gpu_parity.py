@@ -335,7 +335,7 @@ def run_conv(hf, ifm_codes, w_codes, stride, pad, wE, wi, wa, wo, act, algo=0, r
 
 
 @pytest.mark.parametrize("rnd", [0, 1], ids=["rne", "rtz"])
-@pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
+@pytest.mark.parametrize("algo", [1, 2, 3], ids=["fused", "split", "compact"])
 def test_conv_every_product_pair(algo, rnd):
     """A one-tap convolution whose IFM positions are all 2^11 codes of (5,3)
     and whose kernels are all 2^11 codes too: every (w, x) pair through the
@@ -363,7 +363,7 @@ def test_small_conv_workload():
     assert np.array_equal(got, want)
 
 
-@pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
+@pytest.mark.parametrize("algo", [1, 2, 3], ids=["fused", "split", "compact"])
 @pytest.mark.parametrize("v", variants.CONV_VARIANTS, ids=variants.conv_tag)
 def test_conv_variants_vs_oracle(v, algo):
     """Every generated variant, in both kernel shapes, on a problem spanning two
@@ -372,6 +372,8 @@ def test_conv_variants_vs_oracle(v, algo):
     wE, wi, wa, wo, act, rnd = v
     d0 = hf.conv_desc(1, 3, 3, 1, 1, 1, 1, 1, 0, (wE, wi), (wE, wa), (wE, wo), act, algo, round=rnd)
     if not hf.conv2d_supported(d0):
+        if algo == hf.ALGO_SPLIT_COMPACT:
+            pytest.skip("variant generated without the compact split kernel (registers)")
         assert algo == hf.ALGO_SPLIT and hf.netlist_ops((wE, wi), (wE, wa), rnd)["mul"] == 0
         pytest.skip("variant generated without the split kernel (registers)")
     g = np.random.default_rng([11, wi, wa, wo, act, rnd])
@@ -387,7 +389,32 @@ def test_conv_variants_vs_oracle(v, algo):
         assert bad.size == 0, f"{len(bad)} mismatches, first at {bad[0]}"
 
 
-@pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
+def test_auto_kernel_choice():
+    """AUTO's kernel shape by chain waves (64 positions of one 32-kernel tile)
+    per SIMD: at most one, the split kernel (the bench layer, 784); up to two,
+    its compact form (stack layer 1, 1,568) or, where that was not generated,
+    the split kernel (stack layer 2's formats); more, the fused kernel (the
+    4x224x224x3 layer, 6,272)."""
+    hf = need_gpu()
+    simds = 4 * torch.cuda.get_device_properties(0).multi_processor_count
+    cases = [((8, 56, 56, 64, 64), (5, 3), (5, 4), (5, 4), 0, 784),
+             ((16, 56, 56, 64, 64), (5, 3), (5, 4), (5, 5), 1, 1568),
+             ((16, 56, 56, 64, 64), (5, 5), (5, 6), (5, 3), 1, 1568),
+             ((4, 224, 224, 3, 64), (5, 3), (5, 4), (5, 4), 0, 6272)]
+    for (N, H, W, C, M), fi, fa, fo, act, chains in cases:
+        d = hf.conv_desc(N, H, W, C, M, 3, 3, 1, 1, fi, fa, fo, act, hf.ALGO_AUTO)
+        compact = hf.conv2d_supported(hf.conv_desc(N, H, W, C, M, 3, 3, 1, 1, fi, fa, fo, act,
+                                                   hf.ALGO_SPLIT_COMPACT))
+        want = (hf.ALGO_SPLIT if chains <= simds else
+                (hf.ALGO_SPLIT_COMPACT if compact else hf.ALGO_SPLIT) if chains <= 2 * simds
+                else hf.ALGO_FUSED)
+        assert hf.conv2d_algo(d) == want, (N, H, W, C, M, fi, fa)
+    if simds == 1024:  # MI355X: the shapes above land in each regime
+        assert [hf.conv2d_algo(hf.conv_desc(N, H, W, C, M, 3, 3, 1, 1, fi, fa, fo, act, 0))
+                for (N, H, W, C, M), fi, fa, fo, act, _ in cases] == [2, 3, 2, 1]
+
+
+@pytest.mark.parametrize("algo", [1, 2, 3], ids=["fused", "split", "compact"])
 def test_conv_1x1_and_raw_codes(algo):
     hf = need_gpu()
     qi = I.random_codes(1, (3, 5, 4, 70), 11).astype(np.uint64)
@@ -398,7 +425,7 @@ def test_conv_1x1_and_raw_codes(algo):
     assert np.array_equal(got, want)
 
 
-@pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
+@pytest.mark.parametrize("algo", [1, 2, 3], ids=["fused", "split", "compact"])
 def test_conv_tap_counts_not_multiple_of_batch(algo):
     """C = 3 with a 3x3 kernel (27 taps) and C = 5 with 1x1 (5 taps): batches and
     channel words end at different taps."""
@@ -412,7 +439,7 @@ def test_conv_tap_counts_not_multiple_of_batch(algo):
         assert np.array_equal(got, orc.conv2d(qi, qw, 1, pad, 5, 3, 4, 4))
 
 
-@pytest.mark.parametrize("algo", [1, 2], ids=["fused", "split"])
+@pytest.mark.parametrize("algo", [1, 2, 3], ids=["fused", "split", "compact"])
 @pytest.mark.parametrize("M", [64, 40, 37])
 def test_conv_fused_unpack(algo, M):
     """The unpack fused into the epilogue (ofm_kind F32 / CODE) equals the

@@ -20,33 +20,38 @@ from paper_2007_06563_amd import inputs as I
 pytestmark = pytest.mark.gpu
 
 
-def _layer(hf):
+ALGOS = pytest.mark.parametrize("algo", [2, 3], ids=["split", "compact"])
+
+
+def _layer(hf, algo):
     s = I.RESNET_CONV_SHAPE
     ifm, w = I.resnet_conv_inputs()
     pi, pw = hf.pack_batch([dev(ifm.reshape(-1, s.C)), dev(w.reshape(-1, s.M))], (5, 3))
     d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, (5, 3), (5, 4), (5, 4),
-                     hf.ACT_NONE, hf.ALGO_SPLIT, ofm_kind=hf.OFM_CODE)
+                     hf.ACT_NONE, algo, ofm_kind=hf.OFM_CODE)
     return s, ifm, w, pi, pw, d
 
 
-def test_default_bound_never_gives_up():
+@ALGOS
+def test_default_bound_never_gives_up(algo):
     hf = need_gpu()
-    s, ifm, w, pi, pw, d = _layer(hf)
+    s, ifm, w, pi, pw, d = _layer(hf, algo)
     hf.wait_failures(reset=True)
-    say("split kernel, default wait bound, 8x56x56x64->64")
+    say(f"split kernel (algo {algo}), default wait bound, 8x56x56x64->64")
     for _ in range(3):
         hf.conv2d(pi, pw, d)
     assert hf.wait_failures(reset=True) == 0
 
 
-def test_zero_bound_give_ups_are_counted():
+@ALGOS
+def test_zero_bound_give_ups_are_counted(algo):
     hf = need_gpu()
-    s, ifm, w, pi, pw, d = _layer(hf)
+    s, ifm, w, pi, pw, d = _layer(hf, algo)
     default = hf.get_wait_limit()
     hf.wait_failures(reset=True)
     try:
         hf.set_wait_limit(0)
-        say("split kernel, wait bound 0 (waits give up), 8x56x56x64->64")
+        say(f"split kernel (algo {algo}), wait bound 0 (waits give up), 8x56x56x64->64")
         hf.conv2d(pi, pw, d)
         gave = hf.wait_failures(reset=True)
     finally:

@@ -11,6 +11,8 @@ Each workload runs whole on the GPU through the C ABI, at its real shape:
     every generated MAC type of the type sweep: every output;
   * the mantissa sweep: 4x224x224x3 -> 64 and 4x28x28x256 -> 512, 3x3, for
     input formats (5, m), m = 2..10, accumulating in (5, m+1): a sample;
+  * the 13-layer stack's first layer in all four kernel shapes: every output
+    equal across them, a sample against the oracle;
   * the 13-layer ResNet-shaped stack at batch 16, planes kept on the GPU from
     layer to layer, ReLU and a format change in every epilogue: a sample.
 Where the oracle recomputes a sample, it takes every border position of every
@@ -124,6 +126,32 @@ def test_resnet_layer_every_output():
     assert bad.size == 0, f"{len(bad)} mismatching codes of {want.size}; first at {bad[0]}"
     want_f = threaded(orc.decode_f32, want, fixed=(5, 4)).view(np.uint32)
     assert np.array_equal(vals[hf.OFM_F32], want_f)
+
+
+def test_stack_layer_one_every_kernel_shape():
+    """The 13-layer stack's first layer (16x56x56x64 -> 64, 3x3, (5,3) ->
+    (5,4) -> (5,5) ReLU: 1,568 chain waves, between one and two per SIMD, so
+    AUTO runs the compact split kernel): the four kernel shapes give the same
+    codes at every output, and those codes match the oracle on every border
+    position plus random points."""
+    hf = need_gpu()
+    s = I.resnet_stack_shapes(16)[0]
+    ifm, w = I.conv_inputs(I.RESNET_STACK, 0, s)
+    qi, qw = orc.quantize_f32(ifm, 5, 3), orc.quantize_f32(w, 5, 3)
+    d = hf.conv_desc(s.N, s.H, s.W, s.C, s.M, s.KH, s.KW, s.stride, s.pad, (5, 3), (5, 4), (5, 5),
+                     1, hf.ALGO_AUTO)
+    assert hf.conv2d_algo(d) == hf.ALGO_SPLIT_COMPACT
+    outs = {}
+    for algo in (hf.ALGO_AUTO, hf.ALGO_FUSED, hf.ALGO_SPLIT, hf.ALGO_SPLIT_COMPACT):
+        say(f"stack layer 1 16x56x56x64->64 algo={algo}")
+        outs[algo] = conv_codes_of(hf, qi, qw, s.stride, s.pad, 5, 3, 4, 5, 1, algo, 0)
+    for algo, o in outs.items():
+        assert np.array_equal(o, outs[hf.ALGO_AUTO]), f"algo {algo} differs from AUTO"
+    pts = sample_points((s.N, s.OH, s.OW), s.M, np.random.default_rng(41), 8192)
+    want = orc.conv2d_points(qi, qw, pts, s.stride, s.pad, 5, 3, 4, 5, 1)
+    got = outs[hf.ALGO_AUTO][pts[:, 0], pts[:, 1], pts[:, 2], pts[:, 3]]
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{bad.size} mismatches; first at {pts[bad[0]]}"
 
 
 def _type_sweep_variants():
