@@ -47,8 +47,8 @@
  *    unpack fused into the last layer's epilogue, Sec. 3.4);
  *  - hobflops_netlist_ops reports the fused MAC, the multiplier, the
  *    accumulating adder and the element-wise MAC separately;
- *  - hobflops_pack_batch, hobflops_avgpool and the *_supported queries are
- *    additions.
+ *  - hobflops_pack_batch, hobflops_avgpool, hobflops_conv2d_algo and the
+ *    *_supported queries are additions.
  */
 #ifndef HOBFLOPS_H
 #define HOBFLOPS_H
