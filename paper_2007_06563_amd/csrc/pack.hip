@@ -69,20 +69,31 @@ __device__ __forceinline__ int64_t value_index(int64_t q, int j, int G, int64_t 
 // the word whose bit i is bit j of lane i's x. Five stages d = 16, 8, 4, 2, 1
 // swap the off-diagonal d x d blocks of lane pairs (j, j ^ d): the lower lane
 // takes its partner's bits i (i & d == 0) into positions i + d, the upper one
-// its partner's bits i + d into positions i. A stage is one cross-lane read
-// (ds_swizzle, xor mode, no memory access), one rotate and one bit select; the
-// per-lane rotate amounts and masks are set up once (lane_transpose_setup).
-// The bit select is one v_bitop3_b32 (truth table 0xCA: mask ? r : x).
-struct LaneT {
-  uint32_t rot[5], mask[5];
+// its partner's bits i + d into positions i. The stages act on disjoint pairs
+// of (lane bit, word bit) coordinates, so they may run in any order.
+//
+// No stage goes through LDS. The stages d = 8, 4, 2, 1 stay inside 16-lane
+// rows: a DPP move brings the partner's word (row rotate by 8, quad
+// permutes, and for d = 4 a mirror of each 8 lanes followed by the quad
+// permute j ^ 3), then one rotate and one bit select (v_bitop3_b32, truth
+// table 0xCA: mask ? r : x) with per-lane rotate amounts and masks set up once
+// (row_transpose_setup). The stage d = 16 pairs rows 0-1 and 2-3 of a wave;
+// it takes two words a, b at once: v_permlane16_swap_b32 gives every lane of
+// row 0 the words of a's lanes j and j + 16 and every lane of row 1 those of
+// b's, and two byte permutes form P (low halves) and Q (high halves). After
+// it, row 0 (2) of P holds a's result at lanes 0-15 of its half and row 0 (2)
+// of Q a's result at lanes 16-31, rows 1 and 3 the same for b ("pair
+// layout"); a second swap of P and Q gives back the plain layout.
+struct RowT {
+  uint32_t rot[4], mask[4];  // stages d = 8, 4, 2, 1
 };
 
-__device__ __forceinline__ LaneT lane_transpose_setup(int j) {
-  LaneT t;
-  constexpr uint32_t kLow[5] = {0x0000FFFFu, 0x00FF00FFu, 0x0F0F0F0Fu, 0x33333333u, 0x55555555u};
+__device__ __forceinline__ RowT row_transpose_setup(int j) {
+  RowT t;
+  constexpr uint32_t kLow[4] = {0x00FF00FFu, 0x0F0F0F0Fu, 0x33333333u, 0x55555555u};
 #pragma unroll
-  for (int s = 0; s < 5; ++s) {
-    const int d = 16 >> s;
+  for (int s = 0; s < 4; ++s) {
+    const int d = 8 >> s;
     const bool upper = (j & d) != 0;
     t.rot[s] = upper ? d : 32 - d;               // rotate right: by d, or left by d
     t.mask[s] = upper ? kLow[s] : ~kLow[s];      // the positions taken from the partner
@@ -90,20 +101,29 @@ __device__ __forceinline__ LaneT lane_transpose_setup(int j) {
   return t;
 }
 
+// The word of lane j ^ (8 >> S) of the same 16-lane row (DPP moves).
 template <int S>
-__device__ __forceinline__ uint32_t xor_lane(uint32_t x) {
-  constexpr int d = 16 >> S;
-  // bit-mask mode: source lane ((i & 31) | 0) ^ d within each 32 lanes
-  return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, (d << 10) | 0x1F);
+__device__ __forceinline__ uint32_t row_xor(uint32_t x) {
+  if constexpr (S == 0) {
+    return __builtin_amdgcn_mov_dpp(x, 0x128, 0xF, 0xF, false);  // row_ror:8
+  } else if constexpr (S == 1) {
+    const uint32_t m = __builtin_amdgcn_mov_dpp(x, 0x141, 0xF, 0xF, false);  // j ^ 7
+    return __builtin_amdgcn_mov_dpp(m, 0x1B, 0xF, 0xF, false);  // quad_perm [3,2,1,0]: j ^ 3
+  } else if constexpr (S == 2) {
+    return __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+  } else {
+    return __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+  }
 }
 
-template <int U>
-__device__ __forceinline__ void lane_transpose(uint32_t (&x)[U], const LaneT& t) {
+// The stages d = 8, 4, 2, 1 on N words.
+template <int N>
+__device__ __forceinline__ void row_transpose(uint32_t (&x)[N], const RowT& t) {
 #define HOBFLOPS_STAGE(S)                                                       \
   {                                                                             \
-    uint32_t p[U];                                                              \
-    _Pragma("unroll") for (int u = 0; u < U; ++u) p[u] = xor_lane<S>(x[u]);     \
-    _Pragma("unroll") for (int u = 0; u < U; ++u) {                             \
+    uint32_t p[N];                                                              \
+    _Pragma("unroll") for (int u = 0; u < N; ++u) p[u] = row_xor<S>(x[u]);      \
+    _Pragma("unroll") for (int u = 0; u < N; ++u) {                             \
       const uint32_t r = __builtin_amdgcn_alignbit(p[u], p[u], t.rot[S]);       \
       x[u] = __builtin_amdgcn_bitop3_b32(t.mask[S], r, x[u], 0xCA);             \
     }                                                                           \
@@ -112,8 +132,69 @@ __device__ __forceinline__ void lane_transpose(uint32_t (&x)[U], const LaneT& t)
   HOBFLOPS_STAGE(1)
   HOBFLOPS_STAGE(2)
   HOBFLOPS_STAGE(3)
-  HOBFLOPS_STAGE(4)
 #undef HOBFLOPS_STAGE
+}
+
+// Exchanges rows 1 and 3 of a with rows 0 and 2 of b.
+__device__ __forceinline__ void row_swap(uint32_t& a, uint32_t& b) {
+  const auto s = __builtin_amdgcn_permlane16_swap(a, b, false, false);
+  a = s[0];
+  b = s[1];
+}
+
+// Low and high 16-bit halves of two words: lo = lo16(a) | lo16(b) << 16,
+// hi = hi16(a) | hi16(b) << 16.
+__device__ __forceinline__ uint32_t halves_lo(uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_perm(b, a, 0x05040100u);
+}
+__device__ __forceinline__ uint32_t halves_hi(uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_perm(b, a, 0x07060302u);
+}
+
+// The stage d = 16 on words a, b in the plain layout; P and Q in the pair
+// layout. kHigh false: the words' high halves are zero and Q (then zero) is
+// not formed.
+template <bool kHigh>
+__device__ __forceinline__ void stage16_to_pairs(uint32_t a, uint32_t b, uint32_t& P,
+                                                 uint32_t& Q) {
+  row_swap(a, b);
+  P = halves_lo(a, b);
+  if constexpr (kHigh) Q = halves_hi(a, b);
+}
+
+// The stage d = 16 on words held in the pair layout, results in the plain
+// layout (the stage applied to the plain words that P and Q stand for).
+__device__ __forceinline__ void stage16_from_pairs(uint32_t P, uint32_t Q, uint32_t& a,
+                                                   uint32_t& b) {
+  a = halves_lo(P, Q);
+  b = halves_hi(P, Q);
+  row_swap(a, b);
+}
+
+// Whole transpose, plain layout in and out, of U (even) words.
+template <int U>
+__device__ __forceinline__ void lane_transpose(uint32_t (&x)[U], int j) {
+  static_assert(U % 2 == 0, "words go through the d = 16 stage in pairs");
+  uint32_t P[U / 2], Q[U / 2];
+#pragma unroll
+  for (int v = 0; v < U / 2; ++v) stage16_to_pairs<true>(x[2 * v], x[2 * v + 1], P[v], Q[v]);
+  const RowT t = row_transpose_setup(j);
+  row_transpose(P, t);
+  row_transpose(Q, t);
+#pragma unroll
+  for (int v = 0; v < U / 2; ++v) {
+    row_swap(P[v], Q[v]);
+    x[2 * v] = P[v];
+    x[2 * v + 1] = Q[v];
+  }
+}
+
+// Group (within the pass set) and first plane of a lane's word of pair v in
+// the pair layout: row r of a pair of passes (2v, 2v + 1) holds group
+// 2 (2v + (r & 1)) + (r >> 1).
+__device__ __forceinline__ int pair_group(int v, int lane) {
+  const int r = lane >> 4;
+  return 4 * v + 2 * (r & 1) + (r >> 1);
 }
 
 // A pack launch covers up to kMaxJobs ranges of groups, each of one tensor
@@ -190,8 +271,9 @@ __device__ __forceinline__ void quantize_all(uint32_t (&x)[U], const bool (&have
 // for a load count only the loads before it. A range's last groups that do
 // not fill a chunk form a range of their own (the per-value path). LDS
 // operations of one wave complete in order, so only the compiler needs to be
-// kept from reordering them (wave barriers).
-constexpr int kChunksPerWave = 2;
+// kept from reordering them (wave barriers). Four chunks a wave measured
+// faster than two or eight, for the pack and the unpack alike.
+constexpr int kChunksPerWave = 4;
 
 template <int U>
 struct ChunkRegs {
@@ -221,7 +303,6 @@ __device__ __forceinline__ void pack_process_chunk(const PackRange& R, int64_t c
 #pragma unroll
   for (int k = 0; k < U / 4; ++k) reinterpret_cast<lds_u32x4*>(buf)[lane + 64 * k] = r.v[k];
   __builtin_amdgcn_wave_barrier();
-  const int j = lane & 31, h = lane >> 5;
   uint32_t x[U];
   bool have[U];
 #pragma unroll
@@ -231,10 +312,23 @@ __device__ __forceinline__ void pack_process_chunk(const PackRange& R, int64_t c
   }
   __builtin_amdgcn_wave_barrier();  // every value read before the buffer is rewritten
   quantize_all<NB, U>(x, have, R.kind, wE, wF);
-  lane_transpose(x, lane_transpose_setup(j));
+  // the transpose, left in the pair layout: codes of NB <= 16 bits have no
+  // high halves, and then the planes 16-31 (Q) are neither formed nor kept
+  constexpr bool kHigh = NB > 16;
+  uint32_t P[U / 2], Q[U / 2];
 #pragma unroll
-  for (int u = 0; u < U; ++u)
-    if (j < NB) buf[(2 * u + h) * NB + j] = x[u];
+  for (int v = 0; v < U / 2; ++v) stage16_to_pairs<kHigh>(x[2 * v], x[2 * v + 1], P[v], Q[v]);
+  const RowT t = row_transpose_setup(lane & 15);
+  row_transpose(P, t);
+  if constexpr (kHigh) row_transpose(Q, t);
+  const int l = lane & 15;
+#pragma unroll
+  for (int v = 0; v < U / 2; ++v) {
+    const int g = pair_group(v, lane);
+    if (l < NB) buf[g * NB + l] = P[v];
+    if constexpr (kHigh)
+      if (16 + l < NB) buf[g * NB + 16 + l] = Q[v];
+  }
   __builtin_amdgcn_wave_barrier();
   u32x4* dst = reinterpret_cast<u32x4*>(R.planes + qw0 * NB);
 #pragma unroll
@@ -245,8 +339,12 @@ __device__ __forceinline__ void pack_process_chunk(const PackRange& R, int64_t c
   }
 }
 
+// Eight waves a SIMD (at most 64 VGPRs): the compiler then keeps a few
+// values in scratch, and the launch still runs faster than at the six waves
+// its free choice of about 76 VGPRs allows.
 template <int NB, int U>
-__global__ __launch_bounds__(256) void pack_kernel(const PackLaunch L, int wE, int wF) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void pack_kernel(
+    const PackLaunch L, int wE, int wF) {
   const int lane = threadIdx.x & 63;
   // the wave index as a wave-uniform value, so that the range lookup, the
   // range's fields and the mode branches stay scalar
@@ -290,7 +388,7 @@ __global__ __launch_bounds__(256) void pack_kernel(const PackLaunch L, int wE, i
   // one uniform branch for the whole pass set
   quantize_all<NB, U>(x, have, R.kind, wE, wF);
   // lane j of each half now holds plane j of its group
-  lane_transpose(x, lane_transpose_setup(j));
+  lane_transpose(x, j);
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int64_t q = R.q0 + ((wave - R.wave0) * U + u) * 2 + (lane >> 5);
@@ -340,15 +438,29 @@ __device__ __forceinline__ void unpack_process_chunk(int64_t nchunks, int64_t ch
     if (kUnits % 64 == 0 || unit < kUnits) reinterpret_cast<lds_u32x4*>(buf)[unit] = r.v[k];
   }
   __builtin_amdgcn_wave_barrier();
-  const int j = lane & 31, h = lane >> 5;
-  uint32_t x[U];
+  // the plane words come in in the pair layout (planes 16-31 only when NB > 16)
+  constexpr bool kHigh = NB > 16;
+  const int l = lane & 15;
+  uint32_t P[U / 2], Q[U / 2];
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const uint32_t v = buf[(2 * u + h) * NB + min(j, NB - 1)];
-    x[u] = j < NB ? v : 0u;
+  for (int v = 0; v < U / 2; ++v) {
+    const int g = pair_group(v, lane);
+    const uint32_t w = buf[g * NB + min(l, NB - 1)];
+    P[v] = l < NB ? w : 0u;
+    if constexpr (kHigh) {
+      const uint32_t w2 = buf[g * NB + min(16 + l, NB - 1)];
+      Q[v] = 16 + l < NB ? w2 : 0u;
+    } else {
+      Q[v] = 0u;
+    }
   }
   __builtin_amdgcn_wave_barrier();  // every word read before the buffer is rewritten
-  lane_transpose(x, lane_transpose_setup(j));
+  const RowT t = row_transpose_setup(l);
+  row_transpose(P, t);
+  if constexpr (kHigh) row_transpose(Q, t);
+  uint32_t x[U];
+#pragma unroll
+  for (int v = 0; v < U / 2; ++v) stage16_from_pairs(P[v], Q[v], x[2 * v], x[2 * v + 1]);
   decode_all<U>(x, kind, wE, wF);
 #pragma unroll
   for (int u = 0; u < U; ++u) buf[64 * u + lane] = x[u];
@@ -393,7 +505,7 @@ __global__ __launch_bounds__(256) void unpack_kernel(const uint32_t* __restrict_
     x[u] = j < NB ? v : 0u;
   }
   // the transpose is its own inverse: lane j now holds the code at column 32g + j
-  lane_transpose(x, lane_transpose_setup(j));
+  lane_transpose(x, j);
   decode_all<U>(x, kind, wE, wF);
 #pragma unroll
   for (int u = 0; u < U; ++u) {
