@@ -47,29 +47,31 @@ __device__ __forceinline__ uint32_t quantize_bits(uint32_t bits, int wE, int wF)
 // 2^(u - wF) in its binade and |x| + C stays in that binade, so the float32
 // add rounds |x| to wF fraction bits, ties to even (the multiple index of C
 // is even), and subtracting C again is exact; a round-up into the next
-// binade shows in the result's exponent. The exponent field then moves by
-// the bias difference, and the sign of t tells an underflow. |x| is clamped
-// to 2^100, which every such format overflows, so that C stays finite; NaN is
-// tested on the input. The three special cases are selected with all-ones
-// masks (arithmetic shifts of a difference's sign), each in one v_bitop3_b32
-// (truth table 0xCA: mask ? a : b).
+// binade shows in the result's exponent. The rounded magnitude r, read as
+// an integer, orders like the value, so the range tests compare r with the
+// bit patterns of the format's smallest normal and of its overflow
+// threshold, and (r >> k) rebiased is the code's E and F fields. |x| is
+// clamped to 2^100, which every such format overflows, so that C stays
+// finite; NaN is tested on the input. The special cases are per-lane selects
+// (v_cndmask_b32) of uniform constants, and the sign goes in last, except on
+// NaN.
 __device__ __forceinline__ uint32_t quantize_narrow(uint32_t bits, int wE, int wF) {
   const uint32_t a = bits & 0x7FFFFFFFu;
   const uint32_t ac = min(a, 0x71800000u);
   const int k = 23 - wF;
   const float C = __uint_as_float((ac & 0x7F800000u) + ((uint32_t)k << 23));
-  const float r = __fsub_rn(__fadd_rn(__uint_as_float(ac), C), C);
+  const uint32_t r = __float_as_uint(__fsub_rn(__fadd_rn(__uint_as_float(ac), C), C));
   const int bias = (1 << (wE - 1)) - 1;
-  const int t = (int)(__float_as_uint(r) >> k) - ((127 - bias) << wF);
-  const int sh_x = wF + wE + 1;
-  const uint32_t sgn = (bits >> 31) << (wF + wE);
-  const uint32_t under = (uint32_t)(t >> 31);                           // t < 0
-  const uint32_t over = (uint32_t)(((1 << (wE + wF)) - 1 - t) >> 31);   // t >= 2^(wE+wF)
-  const uint32_t nan = (uint32_t)((int)(0x7F800000u - a) >> 31);        // a > 0x7F800000
-  uint32_t code = (1u << sh_x) | sgn | (uint32_t)t;
-  code = __builtin_amdgcn_bitop3_b32(under, sgn, code, 0xCA);                   // +-0
-  code = __builtin_amdgcn_bitop3_b32(over, (2u << sh_x) | sgn, code, 0xCA);     // +-inf
-  return __builtin_amdgcn_bitop3_b32(nan, 3u << sh_x, code, 0xCA);              // NaN
+  const int sh_s = wF + wE, sh_x = sh_s + 1;
+  const uint32_t base = (uint32_t)(127 - bias) << wF;                // E = 0 in r >> k
+  const uint32_t lo = base << k;                                    // smallest normal
+  const uint32_t hi = lo + (1u << (sh_s + k));                      // first overflowing value
+  // (1 << sh_x) | t for the fields t = (r >> k) - base of a value in range
+  uint32_t code = (r >> k) + ((1u << sh_x) - base);
+  code = r < lo ? 0u : code;                                        // +-0
+  code = r >= hi ? (2u << sh_x) : code;                             // +-inf
+  code |= (bits >> (31 - sh_s)) & (1u << sh_s);                     // the sign
+  return a > 0x7F800000u ? (3u << sh_x) : code;                     // NaN
 }
 
 // code of (wE, wF) -> float32 bits for wE <= 7, where every value of the
