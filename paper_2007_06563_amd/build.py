@@ -112,7 +112,8 @@ def _save_circuit_cache():
 
 # Netlists whose results may be non-canonical (they feed only the adder and
 # the accumulator), so that E and F of a non-normal result and the sign of a
-# NaN are free: the don't-care pass of gen.opt applies to them.
+# NaN are free: the don't-care and resubstitution passes of gen.opt apply to
+# them.
 _NONCANONICAL = ("accum", "prod")
 _CIRCUITS = {}  # (kind, key, rounding name) -> (optimised circuit, raw node count)
 
@@ -137,10 +138,15 @@ def _build_circuit(kind, key, r):
     C = opt.optimize(C)
     if kind in _NONCANONICAL:
         wE, wFo = key[0], key[-1]
-        D = opt.dont_care_substitute(C, opt.noncanonical_care(wE, wFo))
+        care = opt.noncanonical_care(wE, wFo)
+        D = opt.dont_care_substitute(C, care)
         if D.n_nodes() < C.n_nodes():
             D = opt.optimize(D)
             C = D if D.n_nodes() < C.n_nodes() else C
+        D = opt.resubstitute(C, care)
+        if D.n_nodes() < C.n_nodes():
+            E = opt.optimize(D)
+            C = E if E.n_nodes() < D.n_nodes() else D
     return C, raw
 
 

@@ -261,7 +261,7 @@ __device__ __forceinline__ void quantize_all(uint32_t (&x)[U], const bool (&have
 }
 
 // Dense ranges with 16-byte aligned arrays (kIdxDenseVec), whole chunks of
-// 2U groups (64U values) only: a wave takes kChunksPerWave consecutive chunks
+// 2U groups (64U values) only: a wave takes chunks_per_wave(U) consecutive chunks
 // and keeps the next two chunks' loads in flight while it works on one, so
 // that memory stays busy through the quantiser and the transpose. A chunk's
 // values come in with 16-byte loads, go through this wave's LDS buffer so
@@ -272,8 +272,13 @@ __device__ __forceinline__ void quantize_all(uint32_t (&x)[U], const bool (&have
 // not fill a chunk form a range of their own (the per-value path). LDS
 // operations of one wave complete in order, so only the compiler needs to be
 // kept from reordering them (wave barriers). Four chunks a wave measured
-// faster than two or eight, for the pack and the unpack alike.
-constexpr int kChunksPerWave = 4;
+// faster than two or eight on large launches, for the pack and the unpack
+// alike; launches of fewer groups (U = kUSmall, about 1.5 waves a SIMD at
+// four chunks on a 1.6 M-value tensor) measured faster at two.
+constexpr int kChunksLarge = 4, kChunksSmall = 2;
+__host__ __device__ constexpr int chunks_per_wave(int U) {
+  return U == kULarge ? kChunksLarge : kChunksSmall;
+}
 
 template <int U>
 struct ChunkRegs {
@@ -357,6 +362,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void p
   if (R.idx == kIdxDenseVec) {  // uniform branch
     __shared__ uint32_t stage[4][64 * U > 2 * U * NB ? 64 * U : 2 * U * NB];
     lds_word* buf = (lds_word*)stage[threadIdx.x >> 6];
+    constexpr int kChunksPerWave = chunks_per_wave(U);
     const int64_t c0 = (wave - R.wave0) * kChunksPerWave;
     // two register sets, alternating (the loop is unrolled by two so that no
     // set still being loaded is copied)
@@ -398,7 +404,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(8))) void p
 
 // The unpack of dense tensors with 16-byte aligned arrays, whole chunks of 2U
 // groups only (the mirror of the pack's; the groups after the last whole
-// chunk go to the per-value path): a wave takes kChunksPerWave consecutive
+// chunk go to the per-value path): a wave takes chunks_per_wave(U) consecutive
 // chunks, with the next two chunks' plane words in flight while it works on
 // one. A chunk's words come in with 16-byte loads, go through LDS so that
 // each lane takes plane j of its half's group per pass, and after the
@@ -482,6 +488,7 @@ __global__ __launch_bounds__(256) void unpack_kernel(const uint32_t* __restrict_
     __shared__ uint32_t stage[4][64 * U > 2 * U * NB ? 64 * U : 2 * U * NB];
     lds_word* buf = (lds_word*)stage[threadIdx.x >> 6];
     const int64_t nchunks = ngroups / (2 * U);
+    constexpr int kChunksPerWave = chunks_per_wave(U);
     const int64_t c0 = __builtin_amdgcn_readfirstlane((int)(wave & 0x7FFFFFFF)) *
                        (int64_t)kChunksPerWave;
     PlaneRegs<NB, U> ra, rb;
@@ -582,7 +589,7 @@ static hipError_t launch_groups(int NB, int64_t len, int64_t ngroups, bool vec,
   const int mode = index_mode(len, ngroups, vec);
   const int64_t chunks = (ngroups + 2 * U - 1) / (2 * U);
   const int64_t waves =
-      mode == kIdxDenseVec ? (chunks + kChunksPerWave - 1) / kChunksPerWave : chunks;
+      mode == kIdxDenseVec ? (chunks + chunks_per_wave(U) - 1) / chunks_per_wave(U) : chunks;
   const int64_t blocks = (waves + 3) / 4;
   if (blocks == 0) return hipSuccess;
   return nb_dispatch<K>::run(NB, [&](auto narrow_k, auto wide_k, auto dense_k, auto vec_k) {
@@ -642,7 +649,7 @@ hipError_t launch_pack_batch(const PackTensor* t, int count, int wE, int wF, hip
       if (qv > q0) {
         L.r[L.count++] = PackRange{t[n].src, t[n].planes, t[n].len, q0, qv, waves, (int)G,
                                    t[n].kind, kIdxDenseVec};
-        waves += ((qv - q0) / (2 * U) + kChunksPerWave - 1) / kChunksPerWave;
+        waves += ((qv - q0) / (2 * U) + chunks_per_wave(U) - 1) / chunks_per_wave(U);
       }
       if (q1 > qv) {
         if (L.count == kMaxJobs) {

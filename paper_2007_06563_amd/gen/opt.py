@@ -22,7 +22,11 @@ one instruction (gfx950 ``v_bitop3_b32``):
   constant or an earlier signal wherever the two differ only on input
   patterns at which no output bit that matters can see the difference. Every
   input pattern is simulated, so the result is exact; it applies to circuits
-  of at most 24 input bits.
+  of at most 24 input bits;
+* resubstitution under the same don't-cares (``resubstitute``): a node whose
+  value, wherever an output bit that matters can see it, is a function of
+  three earlier signals outside its fan-out-free cone becomes one LUT over
+  them, and the cone's other LUTs go. Also exact, also up to 24 input bits.
 """
 import itertools
 
@@ -544,3 +548,147 @@ def noncanonical_care(wE, wF):
         every = np.full_like(x0, np.uint64(0xFFFFFFFFFFFFFFFF))
         return [normal] * (wE + wF) + [notnan, every, every]
     return care
+
+
+def _fanout_lists(C):
+    N = len(C.fanins)
+    lists, counts = {m: [] for m in range(N)}, [0] * N
+    for m in range(1, N):
+        for f in C.fanins[m]:
+            lists[f].append(m)
+            counts[f] += 1
+    for _, lits in C.outputs:
+        for l in lits:
+            counts[l >> 1] += 1
+    return lists, counts
+
+
+def _cone(C, n, counts):
+    """The LUTs of n's maximum fan-out-free cone (n included)."""
+    refs, cone, stack = {}, {n}, [n]
+    while stack:
+        m = stack.pop()
+        for f in C.fanins[m]:
+            if f == 0 or C.is_input[f]:
+                continue
+            refs[f] = refs.get(f, 0) + 1
+            if refs[f] == counts[f]:
+                cone.add(f)
+                stack.append(f)
+    return cone
+
+
+def _function_of(t, care, xs):
+    """Truth table over xs (at most three word arrays) that t follows on the
+    patterns in care, or None; input combinations care never meets are 0."""
+    tt = 0
+    for idx in range(1 << len(xs)):
+        m = care.copy()
+        for i, x in enumerate(xs):
+            m &= x if (idx >> i) & 1 else ~x
+        if not m.any():
+            continue
+        one, zero = (m & t).any(), (m & ~t).any()
+        if one and zero:
+            return None
+        if one:
+            tt |= 1 << idx
+    return tt
+
+
+def _divisor_triples(t, care, V, names):
+    """Triples of rows of V (in row order) that t is a function of on care."""
+    D = V.shape[0]
+    nt, nV = ~t, ~V
+    out = []
+    for i in range(D):
+        for j in range(i + 1, D):
+            ok = np.ones(D, bool)
+            ok[:j + 1] = False
+            for a in (V[i], nV[i]):
+                for b in (V[j], nV[j]):
+                    m = care & a & b
+                    if not m.any():
+                        continue
+                    for c in (V, nV):
+                        M = m & c
+                        ok &= ~((M & t).any(axis=1) & (M & nt).any(axis=1))
+            out.extend((names[i], names[j], names[int(k)]) for k in np.nonzero(ok)[0])
+    return out
+
+
+def resubstitute(C: Circuit, care_fn, max_inputs=24, max_divisors=160, seed=1):
+    """One-LUT resubstitution under output don't-cares (care_fn as for
+    dont_care_substitute). Largest cones first; the candidates come from 512
+    random patterns, are screened on 2^15 more and checked on all 2^inputs
+    patterns before the circuit is rebuilt; every accepted step removes at
+    least one LUT. Divisors are the latest max_divisors earlier signals."""
+    nin = sum(len(l) for _, l in C.inputs)
+    if nin > max_inputs or nin < 6:
+        return C
+    g = np.random.default_rng(seed)
+
+    def sample(count):
+        idx = g.integers(0, 1 << nin, count)
+        planes = []
+        for b in range(nin):
+            bits = ((idx >> b) & 1).astype(np.uint8)
+            planes.append(np.packbits(bits.reshape(-1, 64), axis=1, bitorder="little")
+                          .view(np.uint64).reshape(-1))
+        return planes
+
+    samp, mid, full = sample(512), sample(1 << 15), sim.exhaustive_planes(nin)
+    care = [care_fn(_out_values(C, _node_values(C, p))) for p in (samp, mid, full)]
+    changed = True
+    while changed:
+        changed = False
+        N = len(C.fanins)
+        fo, counts = _fanout_lists(C)
+        vals = [_node_values(C, samp), None, None]
+        outs = [_out_values(C, vals[0]), None, None]
+        order = []
+        for n in range(1, N):
+            if not C.is_input[n]:
+                cone = _cone(C, n, counts)
+                if len(cone) >= 2:
+                    order.append((len(cone), n, cone))
+        order.sort(key=lambda c: (-c[0], c[1]))
+        for _, n, cone in order:
+            seen = _visible(C, vals[0], n, ~vals[0][n], care[0], outs[0], fo)
+            if not seen.any():
+                continue
+            divs = [d for d in range(1, n) if d not in cone][-max_divisors:]
+            cands = _divisor_triples(vals[0][n], seen, np.stack([vals[0][d] for d in divs]), divs)
+            for level in (1, 2):
+                if not cands:
+                    break
+                if vals[level] is None:
+                    vals[level] = _node_values(C, (mid, full)[level - 1])
+                    outs[level] = _out_values(C, vals[level])
+                v = vals[level]
+                seen = _visible(C, v, n, ~v[n], care[level], outs[level], fo)
+                tts = [_function_of(v[n], seen, [v[d] for d in c]) for c in cands]
+                cands = [c for c, tt in zip(cands, tts) if tt is not None]
+                tts = [tt for tt in tts if tt is not None]
+            for c, tt in zip(cands, tts if cands else []):
+                D = Circuit(C.name)
+                m = {0: 0}
+                for group, lits in C.inputs:
+                    for l, nl in zip(lits, D.input(group, len(lits))):
+                        m[l >> 1] = nl
+                for u in range(1, N):
+                    if C.is_input[u]:
+                        continue
+                    if u == n:
+                        m[u] = D.lut(tt, [m[d] for d in c])
+                    else:
+                        m[u] = D.lut(C.tts[u], [m[f] for f in C.fanins[u]])
+                for group, lits in C.outputs:
+                    D.output(group, [m[l >> 1] ^ (l & 1) for l in lits])
+                D = sweep(D)
+                if D.n_nodes() < C.n_nodes():
+                    C, changed = D, True
+                    break
+            if changed:
+                break
+    return C
