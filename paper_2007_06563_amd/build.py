@@ -53,6 +53,7 @@ def _circuit_sources_digest():
     for name in ("circuit.py", "fp.py", "opt.py", "sim.py"):
         h.update(open(os.path.join(HERE, "gen", name), "rb").read())
     h.update(repr(_NONCANONICAL).encode())
+    h.update(_compose_mac.__doc__.encode())  # the fused step's recipe
     return h.hexdigest()[:16]
 
 
@@ -118,11 +119,43 @@ _NONCANONICAL = ("accum", "prod")
 _CIRCUITS = {}  # (kind, key, rounding name) -> (optimised circuit, raw node count)
 
 
-def _build_circuit(kind, key, r):
+def _compose_mac(P, A, key, r):
+    """The fused step acc' = A(acc, P(w, x)) built from the optimised product
+    and accumulating-adder circuits, with the ports of fp.mac_circuit."""
+    from paper_2007_06563_amd.gen.circuit import Circuit
+    wE, wi, wa = key
+    D = Circuit(fp.mac_circuit(wE, wi, wa, rnd=r).name)
+    port = {"acc": D.input("acc", nb(wE, wa)), "w": D.input("w", nb(wE, wi)),
+            "x": D.input("x", nb(wE, wi))}
+
+    def place(C, given):
+        m = {0: 0}
+        for group, lits in C.inputs:
+            for l, nl in zip(lits, given[group]):
+                m[l >> 1] = nl ^ (l & 1)
+        for n in range(1, len(C.fanins)):
+            if not C.is_input[n]:
+                m[n] = D.lut(C.tts[n], [m[f] for f in C.fanins[n]])
+        return {group: [m[l >> 1] ^ (l & 1) for l in lits] for group, lits in C.outputs}
+
+    p = place(P, {"w": port["w"], "x": port["x"]})["p"]
+    D.output("acc", place(A, {"acc": port["acc"], "p": p})["acc"])
+    return opt.sweep(D)
+
+
+def _build_circuit(kind, key, r, parts=None):
     """The operator circuit, optimised and mapped to LUT3 (module level so that
-    a process pool can run it)."""
+    a process pool can run it). For the fused step, `parts` holds the
+    optimised product and adder circuits: their composition (optimised once
+    more across the seam) is kept when it is smaller than the step optimised
+    as one circuit, which is too wide for the exhaustive passes."""
     if kind == "mac":
         C = fp.mac_circuit(*key, rnd=r)
+        if parts is not None:
+            raw = C.n_nodes()
+            C = opt.optimize(C)
+            J = opt.optimize(_compose_mac(*parts, key, r))
+            return (J if J.n_nodes() < C.n_nodes() else C), raw
     elif kind == "prod":
         C = fp.product_circuit(*key, rnd=r)
     elif kind == "accum":
@@ -154,19 +187,35 @@ def circuit(kind, key, r):
     """Optimised circuit of one operator (memoised per process)."""
     k = (kind, tuple(key), r)
     if k not in _CIRCUITS:
-        _CIRCUITS[k] = _build_circuit(kind, key, r)
+        parts = None
+        if kind == "mac":
+            wE, wi, wa = key
+            parts = (circuit("prod", (wE, wi, wa), r)[0], circuit("accum", (wE, wa), r)[0])
+        _CIRCUITS[k] = _build_circuit(kind, key, r, parts)
     return _CIRCUITS[k]
 
 
 def prepare_circuits(needed, jobs=None):
-    """Optimise the circuits in `needed` (kind, key, rounding name) in parallel."""
+    """Optimise the circuits in `needed` (kind, key, rounding name) in parallel:
+    products and adders first, then the fused steps composed from them."""
     todo = [k for k in dict.fromkeys(needed) if k not in _CIRCUITS]
     if not todo:
         return
+    macs = [k for k in todo if k[0] == "mac"]
+    first = [k for k in todo if k[0] != "mac"]
+    for _, (wE, wi, wa), r in macs:
+        first += [k for k in (("prod", (wE, wi, wa), r), ("accum", (wE, wa), r))
+                  if k not in _CIRCUITS and k not in first]
     jobs = jobs or min(16, os.cpu_count() or 4)
     with cf.ProcessPoolExecutor(jobs) as ex:
-        for k, res in zip(todo, ex.map(_build_circuit, *zip(*todo))):
-            _CIRCUITS[k] = res
+        if first:
+            for k, res in zip(first, ex.map(_build_circuit, *zip(*first))):
+                _CIRCUITS[k] = res
+        if macs:
+            parts = [(_CIRCUITS[("prod", key, r)][0], _CIRCUITS[("accum", key[::2], r)][0])
+                     for _, key, r in macs]
+            for k, res in zip(macs, ex.map(_build_circuit, *zip(*macs), parts)):
+                _CIRCUITS[k] = res
 
 
 def _netlist_name(kind, key, rnd):

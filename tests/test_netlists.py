@@ -50,14 +50,16 @@ def random_codes(g, n, wE, wF):
 
 
 _OPT = {}
-_SHIPPED = {"product_circuit": "prod", "accumulate_circuit": "accum"}
+_SHIPPED = {"product_circuit": "prod", "accumulate_circuit": "accum", "mac_circuit": "mac"}
 
 
 def optimized(kind, *args, **kw):
-    """The optimised circuit of a builder, once per session: for the product
-    and the accumulating adder, exactly the library's (build.circuit, with its
-    don't-care and resubstitution passes; taken from the build's circuit cache
-    when its sources match); otherwise opt.optimize of the builder's output."""
+    """The optimised circuit of a builder, once per session: for the product,
+    the accumulating adder and the fused step, exactly the library's
+    (build.circuit, with its don't-care and resubstitution passes and the
+    fused step composed from the other two; taken from the build's circuit
+    cache when its sources match); otherwise opt.optimize of the builder's
+    output."""
     key = (kind, args, tuple(sorted(kw.items())))
     if not _OPT:
         build._load_circuit_cache()  # the shipped circuits, where a build left them
