@@ -162,8 +162,9 @@ __device__ __forceinline__ void stage16_to_pairs(uint32_t a, uint32_t b, uint32_
   if constexpr (kHigh) Q = halves_hi(a, b);
 }
 
-// The stage d = 16 on words held in the pair layout, results in the plain
-// layout (the stage applied to the plain words that P and Q stand for).
+// The stage d = 16 on words a, b given in the pair layout (P: a's lanes 0-15
+// in row 0 and b's in row 1, Q: their lanes 16-31; rows 2 and 3 likewise for
+// the wave's second half); a and b come out in the plain layout.
 __device__ __forceinline__ void stage16_from_pairs(uint32_t P, uint32_t Q, uint32_t& a,
                                                    uint32_t& b) {
   a = halves_lo(P, Q);
@@ -189,9 +190,10 @@ __device__ __forceinline__ void lane_transpose(uint32_t (&x)[U], int j) {
   }
 }
 
-// Group (within the pass set) and first plane of a lane's word of pair v in
-// the pair layout: row r of a pair of passes (2v, 2v + 1) holds group
-// 2 (2v + (r & 1)) + (r >> 1).
+// Group (within the chunk's pass set) of a lane's word of pair v in the pair
+// layout: row r of the passes (2v, 2v + 1) holds group
+// 2 (2v + (r & 1)) + (r >> 1); the lane's plane is lane & 15 in P, 16 more
+// in Q.
 __device__ __forceinline__ int pair_group(int v, int lane) {
   const int r = lane >> 4;
   return 4 * v + 2 * (r & 1) + (r >> 1);
