@@ -80,8 +80,10 @@ __device__ __forceinline__ uint32_t quantize_narrow(uint32_t bits, int wE, int w
 // with masks of the exception bits, without branches.
 __device__ __forceinline__ uint32_t decode_narrow(uint32_t code, int wE, int wF) {
   const int sh_s = wF + wE;
-  const uint32_t e = __builtin_amdgcn_ubfe(code, wF, wE) + (uint32_t)(127 - ((1 << (wE - 1)) - 1));
-  const uint32_t v = (e << 23) | ((code << (23 - wF)) & 0x7FFFFFu);   // the normal value
+  // the normal value: E and F shifted by 23 - wF land on float32's exponent
+  // and fraction fields, and one add rebiases the exponent (it stays below 255)
+  const uint32_t v = (__builtin_amdgcn_ubfe(code, 0, sh_s) << (23 - wF)) +
+                     ((uint32_t)(127 - ((1 << (wE - 1)) - 1)) << 23);
   const uint32_t sbit = (code >> sh_s) << 31;
   const uint32_t x0 = (uint32_t)__builtin_amdgcn_sbfe((int)code, sh_s + 1, 1);  // all ones if set
   const uint32_t x1 = (uint32_t)__builtin_amdgcn_sbfe((int)code, sh_s + 2, 1);
