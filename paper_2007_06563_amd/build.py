@@ -53,7 +53,7 @@ def _circuit_sources_digest():
     for name in ("circuit.py", "fp.py", "opt.py", "sim.py"):
         h.update(open(os.path.join(HERE, "gen", name), "rb").read())
     h.update(repr(_NONCANONICAL).encode())
-    h.update(_compose_mac.__doc__.encode())  # the fused step's recipe
+    h.update(_MAC_RECIPE.encode())
     return h.hexdigest()[:16]
 
 
@@ -117,6 +117,10 @@ def _save_circuit_cache():
 # them.
 _NONCANONICAL = ("accum", "prod")
 _CIRCUITS = {}  # (kind, key, rounding name) -> (optimised circuit, raw node count)
+
+
+# How the fused step's circuit is made (part of the circuit cache's key).
+_MAC_RECIPE = "mac: the smaller of one optimised circuit and product + adder composed"
 
 
 def _compose_mac(P, A, key, r):
