@@ -120,7 +120,8 @@ _CIRCUITS = {}  # (kind, key, rounding name) -> (optimised circuit, raw node cou
 
 
 # How the fused step's circuit is made (part of the circuit cache's key).
-_MAC_RECIPE = "mac: the smaller of one optimised circuit and product + adder composed"
+_MAC_RECIPE = ("mac: the smaller of one optimised circuit and product + adder composed; "
+               "accum: the smaller of both alignment structures")
 
 
 def _compose_mac(P, A, key, r):
@@ -163,7 +164,12 @@ def _build_circuit(kind, key, r, parts=None):
     elif kind == "prod":
         C = fp.product_circuit(*key, rnd=r)
     elif kind == "accum":
-        C = fp.accumulate_circuit(*key, rnd=r)
+        # both structures of the adder's alignment, through every pass; the
+        # smaller is kept
+        A, raw = _optimise_noncanonical(kind, key, fp.accumulate_circuit(*key, rnd=r))
+        B, _ = _optimise_noncanonical(kind, key,
+                                      fp.accumulate_circuit(*key, rnd=r, late_clear=False))
+        return (A if A.n_nodes() <= B.n_nodes() else B), raw
     elif kind == "epi":
         wE, wa, wo, act = key
         C = fp.convert_circuit(wE, wa, wo, relu=bool(act), canonical=True, rnd=r)
@@ -171,6 +177,12 @@ def _build_circuit(kind, key, r, parts=None):
         C = fp.mul_circuit(*key, canonical=True, rnd=r)
     else:
         C = fp.muladd_circuit(*key, rnd=r)
+    return _optimise_noncanonical(kind, key, C)
+
+
+def _optimise_noncanonical(kind, key, C):
+    """Optimised and mapped circuit (with the don't-care and resubstitution
+    passes for the kinds whose results may be non-canonical), raw size."""
     raw = C.n_nodes()
     C = opt.optimize(C)
     if kind in _NONCANONICAL:
