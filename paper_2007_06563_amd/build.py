@@ -121,7 +121,7 @@ _CIRCUITS = {}  # (kind, key, rounding name) -> (optimised circuit, raw node cou
 
 # How the fused step's circuit is made (part of the circuit cache's key).
 _MAC_RECIPE = ("mac: the smaller of one optimised circuit and product + adder composed; "
-               "accum: the smaller of both alignment structures")
+               "accum: the smallest of four alignment structures")
 
 
 def _compose_mac(P, A, key, r):
@@ -164,12 +164,15 @@ def _build_circuit(kind, key, r, parts=None):
     elif kind == "prod":
         C = fp.product_circuit(*key, rnd=r)
     elif kind == "accum":
-        # both structures of the adder's alignment, through every pass; the
-        # smaller is kept
-        A, raw = _optimise_noncanonical(kind, key, fp.accumulate_circuit(*key, rnd=r))
-        B, _ = _optimise_noncanonical(kind, key,
-                                      fp.accumulate_circuit(*key, rnd=r, late_clear=False))
-        return (A if A.n_nodes() <= B.n_nodes() else B), raw
+        # the equivalent structures of the adder's alignment, each through
+        # every pass; the smallest is kept
+        best = None
+        for late_clear, diff_mux in ((True, True), (True, False), (False, True), (False, False)):
+            A, raw = _optimise_noncanonical(kind, key, fp.accumulate_circuit(
+                *key, rnd=r, late_clear=late_clear, diff_mux=diff_mux))
+            if best is None or A.n_nodes() < best[0].n_nodes():
+                best = (A, raw)
+        return best
     elif kind == "epi":
         wE, wa, wo, act = key
         C = fp.convert_circuit(wE, wa, wo, relu=bool(act), canonical=True, rnd=r)

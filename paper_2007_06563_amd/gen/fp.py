@@ -132,12 +132,13 @@ def fp_mul(C: Circuit, A, B, wE, wF, wFo, canonical=True, rnd="rne"):
     return assemble(C, frac, T[:wE], s, nan, inf, is_norm, canonical)
 
 
-def fp_add(C: Circuit, A, B, wE, wF, canonical=True, rnd="rne", late_clear=True):
+def fp_add(C: Circuit, A, B, wE, wF, canonical=True, rnd="rne", late_clear=True,
+           diff_mux=False):
     """(wE, wF) + (wE, wF) -> (wE, wF), rounded once ("rne" or "rtz"; with
     the sticky bit as the sum's least significant bit, truncating the computed
-    sum truncates the exact one). late_clear picks one of two equivalent
-    structures of the alignment (below); the optimiser maps each a little
-    differently."""
+    sum truncates the exact one). late_clear and diff_mux pick between
+    equivalent structures of the alignment (below); the optimiser maps each a
+    little differently."""
     a, b = FP(A, wE, wF), FP(B, wE, wF)
     nan_a, inf_a, zero_a, norm_a = classify(C, a)
     nan_b, inf_b, zero_b, norm_b = classify(C, b)
@@ -157,7 +158,10 @@ def fp_add(C: Circuit, A, B, wE, wF, canonical=True, rnd="rne", late_clear=True)
     # The window is cleared when the smaller operand is zero or shifted out
     # whole: either before the shift (late_clear False) or after it, which
     # gives the same window and sticky bit.
-    d, _ = C.sub(XE, YE)
+    if diff_mux:  # XE - YE as one of the two differences of the unswapped exponents
+        d = C.mux_vec(sw, C.sub(b.E, a.E)[0], C.sub(a.E, b.E)[0])
+    else:
+        d, _ = C.sub(XE, YE)
     nst = (wF + 2).bit_length()
     big = C.OR_all(d[nst:]) if wE > nst else FALSE
     keep = C.AND(nY, NOT(big))
@@ -315,13 +319,13 @@ def product_circuit(wE, wF, wFacc, rnd="rne"):
     return C
 
 
-def accumulate_circuit(wE, wFacc, rnd="rne", late_clear=True):
+def accumulate_circuit(wE, wFacc, rnd="rne", late_clear=True, diff_mux=True):
     """acc' = add(acc, p) for the convolution, non-canonical in and out."""
     C = Circuit(f"accum_e{wE}m{wFacc}{_sfx(rnd)}")
     acc = C.input("acc", nb(wE, wFacc))
     p = C.input("p", nb(wE, wFacc))
     C.output("acc", fp_add(C, acc, p, wE, wFacc, canonical=False, rnd=rnd,
-                           late_clear=late_clear))
+                           late_clear=late_clear, diff_mux=diff_mux))
     return C
 
 
