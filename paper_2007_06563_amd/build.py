@@ -148,7 +148,12 @@ def _compose_mac(P, A, key, r):
     return opt.sweep(D)
 
 
-def _build_circuit(kind, key, r, parts=None):
+# The equivalent structures of the accumulating adder (fp.fp_add's late_clear
+# and diff_mux); the build keeps the smallest after every pass.
+_ACCUM_FORMS = ((True, True), (True, False), (False, True), (False, False))
+
+
+def _build_circuit(kind, key, r, parts=None, form=None):
     """The operator circuit, optimised and mapped to LUT3 (module level so that
     a process pool can run it). For the fused step, `parts` holds the
     optimised product and adder circuits: their composition (optimised once
@@ -165,9 +170,9 @@ def _build_circuit(kind, key, r, parts=None):
         C = fp.product_circuit(*key, rnd=r)
     elif kind == "accum":
         # the equivalent structures of the adder's alignment, each through
-        # every pass; the smallest is kept
+        # every pass; the smallest is kept (form: one structure only)
         best = None
-        for late_clear, diff_mux in ((True, True), (True, False), (False, True), (False, False)):
+        for late_clear, diff_mux in (_ACCUM_FORMS if form is None else [_ACCUM_FORMS[form]]):
             A, raw = _optimise_noncanonical(kind, key, fp.accumulate_circuit(
                 *key, rnd=r, late_clear=late_clear, diff_mux=diff_mux))
             if best is None or A.n_nodes() < best[0].n_nodes():
@@ -225,11 +230,16 @@ def prepare_circuits(needed, jobs=None):
     for _, (wE, wi, wa), r in macs:
         first += [k for k in (("prod", (wE, wi, wa), r), ("accum", (wE, wa), r))
                   if k not in _CIRCUITS and k not in first]
+    # each adder's structures as jobs of their own, reduced to the smallest
+    runs = [(k, None) for k in first if k[0] != "accum"]
+    runs += [(k, f) for k in first if k[0] == "accum" for f in range(len(_ACCUM_FORMS))]
     jobs = jobs or min(16, os.cpu_count() or 4)
     with cf.ProcessPoolExecutor(jobs) as ex:
-        if first:
-            for k, res in zip(first, ex.map(_build_circuit, *zip(*first))):
-                _CIRCUITS[k] = res
+        if runs:
+            args = [k + (None, f) for k, f in runs]
+            for (k, _), res in zip(runs, ex.map(_build_circuit, *zip(*args))):
+                if k not in _CIRCUITS or res[0].n_nodes() < _CIRCUITS[k][0].n_nodes():
+                    _CIRCUITS[k] = res
         if macs:
             parts = [(_CIRCUITS[("prod", key, r)][0], _CIRCUITS[("accum", key[::2], r)][0])
                      for _, key, r in macs]
