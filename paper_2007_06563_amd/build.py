@@ -306,12 +306,26 @@ COMPACT_TOP, COMPACT_BATCH = 128, 2
 COMPACT_BASES = ((32, 48), (24, 48), (32, 56), (24, 40), (32, 40))
 # Variants whose compact kernel the compiler could only fit by spilling
 # registers to scratch (found by build(), which then rebuilds them without
-# the compact form: a spilling kernel would defeat its purpose).
+# the compact form: a spilling kernel would defeat its purpose). The list
+# holds for the generator and kernel sources it was found with; after any
+# change there every variant is tried in the compact form again.
 COMPACT_SPILLS = os.path.join(GEN, "compact_spills.json")
 
 
+def _compact_digest():
+    h = hashlib.sha256(_gen_sources_digest().encode())
+    h.update(open(os.path.join(HERE, "csrc", "kernels.hpp"), "rb").read())
+    return h.hexdigest()[:16]
+
+
 def _compact_excluded():
-    return set(json.load(open(COMPACT_SPILLS))) if os.path.exists(COMPACT_SPILLS) else set()
+    try:
+        d = json.load(open(COMPACT_SPILLS))
+    except (OSError, ValueError):
+        return set()
+    if not isinstance(d, dict) or d.get("digest") != _compact_digest():
+        return set()
+    return set(d["tags"])
 
 
 def split_asm(wE, wi, wa, rnd, cache, compact=False):
@@ -725,7 +739,8 @@ def build(jobs=None, verbose=True):
     spilled = sorted({t for st in stats.values() for t in st.get("compact_spills", [])})
     if spilled:
         # drop the compact form of those variants and compile their sources again
-        json.dump(sorted(_compact_excluded() | set(spilled)), open(COMPACT_SPILLS, "w"))
+        json.dump({"digest": _compact_digest(),
+                   "tags": sorted(_compact_excluded() | set(spilled))}, open(COMPACT_SPILLS, "w"))
         if verbose:
             print("compact split kernel spills registers, left out:", ", ".join(spilled))
         generate(verbose=False)
